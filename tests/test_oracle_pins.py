@@ -1,0 +1,405 @@
+"""Pins of the CPU oracle against facts it does not compute itself.
+
+Each check is chosen so that a plausible mistake in the oracle (a dropped term,
+a wrong sign or index, a transposed operand, a flipped kernel, a misplaced
+activation, a wrong flatten order, a wrong rounding rule) fails at least one:
+
+* brute-force loop nests written from the definition of a 3x3 cross-correlation;
+* torch.nn.functional.conv2d / linear in float64 on the CPU (library routines);
+* closed forms for networks whose conv weights are zero;
+* softmax invariants and exact special cases;
+* quantiser identities and torch's own float8_e4m3fn / bfloat16 conversions.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as TF
+
+import azgen
+import oracle
+from oracle import az_oracle as O
+
+
+def _rng(seed=0):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+# --------------------------------------------------------------------------- #
+# conv3x3
+# --------------------------------------------------------------------------- #
+def _conv_bruteforce(x, w, b):
+    B, C = x.shape[:2]
+    F = w.shape[0]
+    y = np.zeros((B, F, 8, 8))
+    for n in range(B):
+        for f in range(F):
+            for r in range(8):
+                for c in range(8):
+                    s = b[f]
+                    for i in range(C):
+                        for dy in range(3):
+                            for dx in range(3):
+                                rr, cc = r + dy - 1, c + dx - 1
+                                if 0 <= rr < 8 and 0 <= cc < 8:
+                                    s += w[f, i, dy, dx] * x[n, i, rr, cc]
+                    y[n, f, r, c] = s
+    return y
+
+
+def test_conv3x3_matches_bruteforce():
+    g = _rng(1)
+    x = g.standard_normal((2, 3, 8, 8))
+    w = g.standard_normal((4, 3, 3, 3))
+    b = g.standard_normal(4)
+    np.testing.assert_allclose(O.conv3x3(x, w, b), _conv_bruteforce(x, w, b), rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("B,C,F", [(3, 5, 7), (1, 20, 32), (2, 32, 16)])
+def test_conv3x3_matches_torch_conv2d(B, C, F):
+    g = _rng(B * 100 + C)
+    x = g.standard_normal((B, C, 8, 8))
+    w = g.standard_normal((F, C, 3, 3))
+    b = g.standard_normal(F)
+    ref = TF.conv2d(torch.from_numpy(x), torch.from_numpy(w), torch.from_numpy(b), padding=1).numpy()
+    np.testing.assert_allclose(O.conv3x3(x, w, b), ref, rtol=0, atol=1e-12)
+
+
+def test_conv3x3_identity_kernel():
+    g = _rng(2)
+    x = g.standard_normal((2, 6, 8, 8))
+    w = np.zeros((6, 6, 3, 3))
+    w[np.arange(6), np.arange(6), 1, 1] = 1.0
+    np.testing.assert_array_equal(O.conv3x3(x, w), x)
+
+
+@pytest.mark.parametrize("dy,dx", [(0, 0), (0, 2), (2, 1), (1, 0)])
+def test_conv3x3_tap_orientation_and_no_wraparound(dy, dx):
+    # y[r, c] = x[r+dy-1, c+dx-1]: an impulse at (r0, c0) lands at (r0-dy+1, c0-dx+1).
+    for r0, c0 in [(3, 4), (0, 0), (7, 7), (0, 7)]:
+        x = np.zeros((2, 1, 8, 8))
+        x[0, 0, r0, c0] = 1.0
+        w = np.zeros((1, 1, 3, 3))
+        w[0, 0, dy, dx] = 1.0
+        y = O.conv3x3(x, w)
+        exp = np.zeros((2, 1, 8, 8))
+        r, c = r0 - dy + 1, c0 - dx + 1
+        if 0 <= r < 8 and 0 <= c < 8:
+            exp[0, 0, r, c] = 1.0
+        np.testing.assert_array_equal(y, exp)     # nothing leaks into the next board
+
+
+def test_conv3x3_integer_accumulation_is_exact():
+    g = _rng(3)
+    x = g.integers(-127, 128, size=(2, 128, 8, 8)).astype(np.float64)
+    w = g.integers(-127, 128, size=(16, 128, 3, 3)).astype(np.float64)
+    y = O.conv3x3(x, w)
+    ref = TF.conv2d(torch.from_numpy(x).long().double(), torch.from_numpy(w).double(),
+                    padding=1).numpy()
+    exact = _conv_bruteforce(x[:1, :, :, :], w[:2], np.zeros(2))
+    np.testing.assert_array_equal(y, ref)
+    np.testing.assert_array_equal(y[:1, :2], exact)
+    assert np.all(y == np.rint(y))
+
+
+# --------------------------------------------------------------------------- #
+# Whole network against torch's conv2d / linear (float64, CPU)
+# --------------------------------------------------------------------------- #
+def _torch_net(spec, blob, planes, legal):
+    W = {k: torch.from_numpy(np.array(v)) for k, v in O.unpack(spec, blob).items()}
+    x = torch.from_numpy(np.asarray(planes, dtype=np.float64))
+    cap = spec.act_cap
+
+    def a(t):
+        t = torch.relu(t)
+        return torch.clamp(t, max=cap) if cap > 0 else t
+
+    h = a(TF.conv2d(x, W["stem.w"], W["stem.b"], padding=1))
+    for j in range(spec.blocks):
+        t = a(TF.conv2d(h, W[f"w1.{j}"], W[f"b1.{j}"], padding=1))
+        h = a(h + TF.conv2d(t, W[f"w2.{j}"], W[f"b2.{j}"], padding=1))
+    z = TF.conv2d(h, W["policy.w"][:, :, None, None], W["policy.b"]).flatten(1)
+    m = torch.from_numpy(np.asarray(legal) != 0)
+    z = z.masked_fill(~m, -math.inf)
+    p = torch.softmax(z, dim=1)
+    p = torch.nan_to_num(p, nan=0.0)
+    u = TF.conv2d(h, W["value.w"][:, :, None, None], W["value.b"]).flatten(1)
+    if spec.value_conv_relu:
+        u = torch.relu(u)
+    g = torch.relu(TF.linear(u, W["fc1.w"], W["fc1.b"]))
+    v = torch.tanh(TF.linear(g, W["fc2.w"], W["fc2.b"]))[:, 0]
+    return p.numpy(), v.numpy()
+
+
+@pytest.mark.parametrize("cap,vrelu", [(0.0, 0), (6.0, 1)])
+def test_forward_matches_torch_reference_tiny(cap, vrelu):
+    w = azgen.WORKLOADS["tiny_2x32_f32_b16"]
+    spec = azgen.NetShape(20, 2, 32, 73, 64, value_conv_relu=vrelu, act_cap=cap)
+    blob = azgen.make_weights(spec, 77, alpha_fold=False, bf16=False)
+    planes, legal = azgen.make_inputs(w)
+    P, V = oracle.forward(spec, blob, planes, legal)
+    Pt, Vt = _torch_net(spec, blob, planes, legal)
+    np.testing.assert_allclose(P, Pt, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(V, Vt, rtol=0, atol=1e-12)
+
+
+def test_forward_matches_torch_reference_non_square_shapes():
+    # in_planes != filters, policy planes != 73, hidden != 64: a transposed operand
+    # or a swapped dimension cannot pass.
+    spec = azgen.NetShape(13, 3, 24, 11, 40, value_conv_relu=0, act_cap=0.0)
+    blob = azgen.make_weights(spec, 5, alpha_fold=True, bf16=False)
+    g = _rng(9)
+    planes = g.standard_normal((5, 13, 8, 8))
+    legal = (g.random((5, 11 * 64)) < 0.3).astype(np.uint8)
+    P, V = oracle.forward(spec, blob, planes, legal)
+    Pt, Vt = _torch_net(spec, blob, planes, legal)
+    np.testing.assert_allclose(P, Pt, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(V, Vt, rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------- #
+# Closed forms
+# --------------------------------------------------------------------------- #
+def _zero_conv_blob(spec, seed):
+    blob = azgen.make_weights(spec, seed, alpha_fold=False, bf16=False).astype(np.float64)
+    off = 0
+    for name, shp in spec.layer_sizes():
+        n = int(np.prod(shp))
+        if len(shp) == 4:
+            blob[off:off + n] = 0.0
+        off += n
+    return blob
+
+
+@pytest.mark.parametrize("cap", [0.0, 0.25])
+def test_closed_form_with_zero_convolutions(cap):
+    # With every 3x3 weight zero, each layer is its bias: h0 = act(b_s),
+    # t_j = act(b1_j), h_{j+1} = act(h_j + b2_j), all constant over squares.
+    spec = azgen.NetShape(20, 3, 16, 5, 8, value_conv_relu=0, act_cap=cap)
+    blob = _zero_conv_blob(spec, 11)
+    W = O.unpack(spec, blob)
+
+    def a(v):
+        v = max(v, 0.0)
+        return min(v, cap) if cap > 0 else v
+
+    h = [a(v) for v in W["stem.b"]]
+    for j in range(spec.blocks):
+        h = [a(h[f] + W[f"b2.{j}"][f]) for f in range(16)]
+    z_plane = [W["policy.b"][p] + sum(W["policy.w"][p][f] * h[f] for f in range(16))
+               for p in range(5)]
+    u = W["value.b"][0] + sum(W["value.w"][0][f] * h[f] for f in range(16))
+    gk = [max(W["fc1.b"][k] + u * sum(W["fc1.w"][k]), 0.0) for k in range(8)]
+    v = math.tanh(W["fc2.b"][0] + sum(W["fc2.w"][0][k] * gk[k] for k in range(8)))
+
+    g = _rng(4)
+    planes = g.standard_normal((3, 20, 8, 8))
+    legal = np.zeros((3, 5 * 64), dtype=np.uint8)
+    legal[0, [0, 64, 128, 192, 256]] = 1          # one cell per plane
+    legal[1, :] = 1
+    legal[2, [70, 71]] = 1                        # two cells of plane 1
+    P, V = oracle.forward(spec, blob, planes, legal)
+    e = np.exp(np.array(z_plane) - max(z_plane))
+    np.testing.assert_allclose(P[0, [0, 64, 128, 192, 256]], e / e.sum(), rtol=1e-14, atol=0)
+    np.testing.assert_allclose(P[1].reshape(5, 64), np.repeat((e / e.sum() / 64)[:, None], 64, 1),
+                               rtol=1e-13, atol=0)
+    assert P[2, 70] == P[2, 71] == 0.5
+    np.testing.assert_allclose(V, v, rtol=0, atol=1e-15)
+
+
+def test_policy_flatten_order_is_plane_row_col():
+    spec = azgen.NetShape(1, 1, 4, 6, 4)
+    W = np.zeros((6, 4))
+    W[3, 2] = 1.0
+    h = np.zeros((1, 4, 8, 8))
+    h[0, 2, 5, 1] = 1.0
+    z = O.policy_logits(h, W, np.zeros(6))
+    assert z.shape == (1, 6 * 64)
+    assert np.argmax(z[0]) == 3 * 64 + 5 * 8 + 1
+    assert np.count_nonzero(z) == 1
+    del spec
+
+
+# --------------------------------------------------------------------------- #
+# Softmax and value invariants
+# --------------------------------------------------------------------------- #
+def test_softmax_invariants():
+    g = _rng(5)
+    z = g.standard_normal((6, 4672)) * 5
+    legal = np.zeros((6, 4672), dtype=np.uint8)
+    for i in range(6):
+        legal[i, g.choice(4672, 20 + 4 * i, replace=False)] = 1
+    legal[3] = 0
+    legal[3, 17] = 1                           # single legal move
+    legal[4] = 0                               # terminal: no legal move
+    P = O.softmax_legal(z, legal)
+    assert np.all(P[legal == 0] == 0.0)
+    for i in (0, 1, 2, 5):
+        assert abs(P[i].sum() - 1.0) < 1e-12
+    assert P[3, 17] == 1.0 and P[3].sum() == 1.0
+    assert np.all(P[4] == 0.0)
+    np.testing.assert_allclose(O.softmax_legal(z + 123.0, legal), P, rtol=1e-12, atol=1e-300)
+    # ordering follows the logits among legal cells
+    for i in (0, 1, 2, 5):
+        idx = np.flatnonzero(legal[i])
+        assert np.all(np.argsort(z[i, idx]) == np.argsort(P[i, idx]))
+
+
+def test_softmax_equal_logits_uniform():
+    z = np.full((2, 4672), 0.7)
+    legal = np.zeros((2, 4672), dtype=np.uint8)
+    legal[0, :32] = 1
+    legal[1, 100:137] = 1
+    P = O.softmax_legal(z, legal)
+    assert np.all(P[0, :32] == 1.0 / 32)
+    np.testing.assert_allclose(P[1, 100:137], 1.0 / 37, rtol=1e-15)
+
+
+def test_value_range_and_zero_head():
+    g = _rng(6)
+    h = np.abs(g.standard_normal((8, 16, 8, 8))) * 50
+    wv, bv = g.standard_normal((1, 16)), g.standard_normal(1)
+    w1, b1 = g.standard_normal((32, 64)), g.standard_normal(32)
+    w2, b2 = g.standard_normal((1, 32)) * 10, g.standard_normal(1)
+    V = O.value_head(h, wv, bv, w1, b1, w2, b2, 0)
+    assert np.all(np.abs(V) <= 1.0)
+    Z = O.value_head(h, wv * 0, bv * 0, w1 * 0, b1 * 0, w2 * 0, b2 * 0, 0)
+    assert np.all(Z == 0.0)
+
+
+def test_batch_independence_and_permutation():
+    w = azgen.WORKLOADS["tiny_2x32_f32_b16"]
+    blob = azgen.workload_weights(w)
+    planes, legal = azgen.make_inputs(w)
+    P, V = oracle.forward(w.shape, blob, planes, legal)
+    perm = _rng(7).permutation(16)
+    Pp, Vp = oracle.forward(w.shape, blob, planes[perm], legal[perm])
+    np.testing.assert_allclose(Pp, P[perm], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(Vp, V[perm], rtol=0, atol=1e-14)
+    P1, V1 = oracle.forward(w.shape, blob, planes[5:6], legal[5:6])
+    np.testing.assert_allclose(P1[0], P[5], rtol=0, atol=1e-14)
+
+
+# --------------------------------------------------------------------------- #
+# Quantisers and rounding
+# --------------------------------------------------------------------------- #
+def test_bf16_rounding_matches_torch():
+    g = _rng(8)
+    x = np.concatenate([g.standard_normal(100000).astype(np.float32),
+                        # exact ties: low 16 bits = 0x8000
+                        (np.arange(1, 2000, dtype=np.uint32) << 16 | 0x8000).view(np.float32)])
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.to_bf16(x), ref)
+    np.testing.assert_array_equal(azgen.round_to_bf16(x).astype(np.float64), ref)
+
+
+def test_int8_quantiser():
+    k = np.arange(-130, 131, dtype=np.float32)
+    q = O.quant_int8(k + np.float32(0.5))
+    exp = np.clip(np.where((k.astype(int) % 2) == 0, k, k + 1), -127, 127)
+    np.testing.assert_array_equal(q, exp)                      # ties to even
+    assert O.quant_int8(np.float32(1e9)) == 127 and O.quant_int8(np.float32(-1e9)) == -127
+    codes = np.arange(-127, 128, dtype=np.float32)
+    s = np.float32(0.0371)
+    np.testing.assert_array_equal(O.quant_int8((codes * s) / s), codes)   # q(dq(q)) = q
+
+
+def test_e4m3_codes_round_trip_and_known_values():
+    codes = np.arange(256)
+    vals = O.e4m3_decode(codes)
+    finite = ~np.isnan(vals)
+    assert finite.sum() == 254
+    np.testing.assert_array_equal(O.e4m3_round(vals[finite]), vals[finite])
+    assert np.nanmax(vals) == 448.0 and np.nanmin(vals) == -448.0
+    assert O.e4m3_decode(1) == 2.0 ** -9 and O.e4m3_decode(8) == 2.0 ** -6
+    # torch's own e4m3fn decode agrees with ours for every finite code
+    t = torch.tensor(codes.astype(np.uint8)).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(t[finite], vals[finite])
+    assert O.e4m3_round(np.array([1000.0, -500.0, 460.0]))[0] == 448.0
+    assert O.e4m3_round(np.array([-500.0]))[0] == -448.0
+
+
+def test_e4m3_rounding_matches_torch():
+    g = _rng(10)
+    x = np.concatenate([g.standard_normal(200000) * s for s in (0.002, 0.05, 1.0, 30.0, 150.0)])
+    x = x.astype(np.float32)
+    x = x[np.abs(x) <= 448]
+    # exact midpoints between neighbouring codes
+    vals = np.unique(O.e4m3_decode(np.arange(0, 127)))
+    mids = ((vals[1:] + vals[:-1]) / 2).astype(np.float32)
+    x = np.concatenate([x, mids, -mids])
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.e4m3_round(x), ref)
+
+
+def test_weight_scales_map_absmax_to_qmax():
+    w = azgen.WORKLOADS["tiny_2x32_f32_b16"]
+    blob = azgen.workload_weights(w)
+    W = O.unpack(w.shape, blob)
+    for fmt in ("int8", "fp8"):
+        s = O.weight_scales(w.shape, blob, fmt).reshape(4, 32)
+        q = O.quantize_weights(W["w1.0"], s[0], fmt)
+        assert np.all(np.abs(q).reshape(32, -1).max(1) == O.qmax(fmt))
+        q = O.quantize_weights(W["w2.1"], s[3], fmt)
+        assert np.all(np.abs(q) <= O.qmax(fmt))
+
+
+@pytest.mark.parametrize("fmt", ["int8", "fp8"])
+def test_fake_quant_converges_to_float_network(fmt):
+    # With scales 2^-12 times finer than absmax the quantised network must agree with
+    # the float network to the rounding error; a structural slip (missing residual,
+    # bias or activation, wrong scale index) would not.
+    w = azgen.WORKLOADS["tiny_2x32_f32_b16"]
+    spec = w.shape
+    blob = azgen.make_weights(spec, 21, alpha_fold=True, bf16=True)
+    planes, legal = azgen.make_inputs(w)
+    P, V = oracle.forward(spec, blob, planes, legal)
+    amax = O.calibrate_absmax(spec, blob, planes)
+    ws = O.weight_scales(spec, blob, fmt)
+    acts = O.act_scales_from_absmax(amax, fmt)
+    Pq, Vq = O.forward_quant(spec, blob, ws, acts, fmt, planes, legal)
+    if fmt == "int8":
+        assert np.abs(Pq - P).max() < 0.1 and np.abs(Vq - V).max() < 0.1
+        # int8 with an extra 7 bits of headroom: activations of 14-bit resolution
+        Pf, Vf = _quant_fine(spec, blob, planes, legal, amax)
+        assert np.abs(Pf - P).max() < 2e-3 and np.abs(Vf - V).max() < 2e-3
+    else:
+        assert np.abs(Pq - P).max() < 0.15 and np.abs(Vq - V).max() < 0.15
+
+
+def _quant_fine(spec, blob, planes, legal, amax):
+    # Same int8 network definition with scales 2^-7 of the calibrated ones and
+    # saturation far away: only rounding remains.
+    ws = O.weight_scales(spec, blob, "int8") / np.float32(128.0)
+    acts = (O.act_scales_from_absmax(amax, "int8") / np.float32(128.0)).astype(np.float32)
+    old = O.INT8_MAX
+    try:
+        O.INT8_MAX = 127.0 * 256
+        return O.forward_quant(spec, blob, ws, acts, "int8", planes, legal)
+    finally:
+        O.INT8_MAX = old
+
+
+def test_fake_quant_record_and_exact_codes():
+    w = azgen.WORKLOADS["tiny_2x32_f32_b16"]
+    spec = w.shape
+    blob = azgen.make_weights(spec, 22, alpha_fold=False, bf16=True)
+    planes, legal = azgen.make_inputs(w)
+    amax = O.calibrate_absmax(spec, blob, planes)
+    ws = O.weight_scales(spec, blob, "int8")
+    acts = O.act_scales_from_absmax(amax, "int8")
+    rec = []
+    O.forward_quant(spec, blob, ws, acts, "int8", planes, legal, record=rec)
+    assert len(rec) == 2 * spec.blocks + 1
+    for q in rec:
+        assert np.all(q == np.rint(q)) and np.all(q >= 0) and np.all(q <= 127)
+    # the calibration tensors of the float network reach the top code
+    assert max(float(q.max()) for q in rec) == 127.0
+
+
+def test_parameter_counts():
+    assert azgen.WORKLOADS["tiny_2x32_f32_b16"].shape.weight_count() == 49451
+    assert azgen.WORKLOADS["net20x128_bf16_b256"].shape.weight_count() == 5944523
+    assert azgen.WORKLOADS["net24x256_bf16_b1024"].shape.weight_count() == 28397643
