@@ -1,0 +1,189 @@
+#!/usr/bin/env python3
+"""Benchmark: positions evaluated per second (policy + value) on one MI355X.
+
+One step is one az_eval_batch call over a whole batch of seeded synthetic
+positions already resident in device memory: the fused stem + residual tower +
+heads + legal-move softmax + tanh value kernel.  Default workload: the 20-block,
+128-filter network (5,944,523 parameters) with int8 residual convolutions,
+batch 1024.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--tiling 0|1|2]
+
+Prints one JSON line on stdout.  --gpus N with N > 1 exits with a message: this
+library evaluates on one GPU (positions are independent; a multi-GPU server
+would run one handle per GPU on its share of the batch).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import azgen  # noqa: E402
+
+CALIB = os.path.join(ROOT, "tests", "golden", "calib_net20x128_seed1004.npz")
+
+# MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
+PEAK = {"bf16": 2.5e15, "int8": 5.0e15, "fp8": 5.0e15, "f32_vec": 157.3e12}
+
+
+def mac_counts(shape):
+    """Algorithmic multiply-accumulates per position, by layer group (no padding)."""
+    C, F, P, H, NB = shape.in_planes, shape.filters, shape.policy_planes, shape.value_hidden, shape.blocks
+    return {
+        "stem": 64 * F * C * 9,
+        "tower": 2 * NB * 64 * F * F * 9,
+        "head_conv": 64 * F * (P + 1),
+        "value_fc": 64 * H + H,
+    }
+
+
+def roofline_peak(shape, dtype):
+    """Composite peak: total FLOP / sum_l FLOP_l / peak(dtype_l), each layer group
+    priced at the unit it runs on."""
+    m = mac_counts(shape)
+    if dtype == "f32":
+        unit = {"stem": "f32_vec", "tower": "f32_vec", "head_conv": "f32_vec", "value_fc": "f32_vec"}
+    else:
+        tower = {"bf16": "bf16", "int8": "int8", "fp8": "fp8"}[dtype]
+        unit = {"stem": "bf16", "tower": tower, "head_conv": "bf16", "value_fc": "f32_vec"}
+    flop = {k: 2.0 * v for k, v in m.items()}
+    t_floor = sum(flop[k] / PEAK[unit[k]] for k in flop)
+    return sum(flop.values()), sum(flop.values()) / t_floor
+
+
+def load_scales(w):
+    if w.dtype not in ("int8", "fp8"):
+        return None, None
+    if w.shape != azgen.WORKLOADS["net20x128_int8_b1024"].shape or w.index != 4:
+        raise SystemExit(f"no stored calibration for workload {w.name}")
+    d = np.load(CALIB, allow_pickle=False)
+    return d[f"w_scales_{w.dtype}"], d[f"act_scales_{w.dtype}"]
+
+
+def cpu_baseline(w, blob, ws, acs, planes, legal, budget_s=12.0, chunk=64):
+    """The oracle (float64 CPU forward; quantised mode for int8/fp8) on a bounded
+    sample of the same workload, chunks of `chunk` positions until budget_s."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import az_oracle as O
+    done, t0 = 0, time.perf_counter()
+    while True:
+        s = done % planes.shape[0]
+        pl, lg = planes[s:s + chunk], legal[s:s + chunk]
+        if w.dtype in ("int8", "fp8"):
+            O.forward_quant(w.shape, blob, ws, acs, w.dtype, pl, lg)
+        else:
+            O.forward(w.shape, blob, pl, lg)
+        done += pl.shape[0]
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": done / el, "unit": "positions/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} positions of the seeded batch in chunks of {chunk}, "
+                      f"{el:.1f} s, float64 numpy/BLAS"
+                      + (f" ({w.dtype} quantised network)" if w.dtype in ("int8", "fp8") else "")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="net20x128_int8_b1024", choices=sorted(azgen.WORKLOADS))
+    ap.add_argument("--tiling", type=int, default=0, choices=(0, 1, 2))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: --gpus {args.gpus} (WORLD_SIZE {world}) requested, but this library "
+              "evaluates on one GPU; run one process per GPU with its own share of the batch.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_37447_amd as az
+
+    w = azgen.WORKLOADS[args.workload]
+    blob = azgen.workload_weights(w)
+    ws, acs = load_scales(w)
+    planes, legal = azgen.make_inputs(w)
+    B = w.batch
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    net = az.az_net_load(az.spec_from_shape(w.shape, B), blob, w.dtype, ws, acs)
+    if args.tiling:
+        az.az_net_set_tiling(net, args.tiling)
+    tiling = az.az_net_tiling_for(net, B)
+    pl = torch.from_numpy(planes).to(dev)
+    lg = torch.from_numpy(legal).to(dev)
+    pol = torch.empty((B, w.shape.n_moves), device=dev)
+    val = torch.empty((B,), device=dev)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    def step():
+        az.az_eval_batch(net, pl.data_ptr(), lg.data_ptr(), B, pol.data_ptr(), val.data_ptr(), sp)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    # sanity: every policy row sums to one, values in range
+    s = pol.sum(dim=1)
+    ok = bool(((s - 1).abs() < 1e-3).all()) and bool((val.abs() <= 1).all())
+    az.az_net_free(net)
+
+    flop_pos, peak = roofline_peak(w.shape, w.dtype)
+    achieved = flop_pos * B / (ms * 1e-3)
+    out = {
+        "metric": "positions evaluated/sec (policy+value), one az_eval_batch per step",
+        "value": B / (ms * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"f32": "f32", "bf16": "bf16", "int8": "int8", "fp8": "fp8_e4m3"}[w.dtype],
+        "data": "synthetic (seeded planes, masks and N(0, 2/fan_in) weights)",
+        "config": {"workload": w.name, "blocks": w.shape.blocks, "filters": w.shape.filters,
+                   "in_planes": w.shape.in_planes, "policy_planes": w.shape.policy_planes,
+                   "value_hidden": w.shape.value_hidden, "batch": B, "tiling": tiling,
+                   "params": w.shape.weight_count(), "flop_per_position": flop_pos},
+        "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
+                     "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": None},
+        "outputs_valid": ok,
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, blob, ws, acs, planes, legal, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

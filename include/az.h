@@ -1,0 +1,170 @@
+/*
+ * az.h - C ABI of the MI355X (gfx950) library that evaluates the residual
+ * policy/value network on batches of search-leaf positions.
+ *
+ * What it computes.  In the paper's self-play loop every new search leaf that
+ * is not terminal is sent to the network; requests from many games are grouped
+ * into one batch and evaluated on the GPU, which returns move priors over the
+ * legal moves and a scalar value (Section 3.3 "One learning cycle", Section 3.6
+ * "Search and self-play", Section 5.2 "Batching and host-side submission").
+ * For each position b of a batch this library computes
+ *
+ *   h      = act(conv3x3(planes[b]) + b_stem)                 stem ("start block")
+ *   t      = act(conv3x3(h) + b1_j)                           block j = 0..blocks-1
+ *   h      = act(h + conv3x3(t) + b2_j)                       (post-activation residual block)
+ *   z[i]   = b_p[p] + sum_f Wp[p][f] * h[f][r][c],  i = p*64 + r*8 + c   (move-plane head)
+ *   P[i]   = exp(z[i] - m) / sum_{k legal} exp(z[k] - m) if legal[b][i] != 0, else 0,
+ *            m = max over legal z; a row with no legal cell is all zero
+ *   u[s]   = b_v + sum_f w_v[f] * h[f][s]   (then ReLU if value_conv_relu)
+ *   V      = tanh(w2 . relu(W1 u + b1) + b2)
+ *
+ * conv3x3 is a stride-1 3x3 cross-correlation with a zero pad of one square on
+ * each 8x8 board; act is ReLU, capped at act_cap when act_cap > 0 (the capped
+ * activation of Section 4.3, "Quantization as an architectural constraint").
+ * Batch normalisation and any residual-branch scale are folded into the
+ * weights by the caller, as the paper does on its deployment copy (Section 4.3,
+ * Appendix D).
+ *
+ * Precision (Section 5.3 "Inference runtimes and precision": most trunk
+ * convolutions in INT8, start block, heads and linear layers at higher
+ * precision):
+ *   AZ_F32       every layer in fp32.
+ *   AZ_BF16      bf16 weights and activations, fp32 accumulation; heads fp32
+ *                accumulation, softmax and value in fp32.
+ *   AZ_INT8      the 2*blocks residual convolutions in int8 with int32
+ *                accumulation: weights quantised per output channel
+ *                (q = sat(rne(w / s_w[f])) in fp32, |q| <= 127), every
+ *                activation tensor between layers stored as int8 codes with a
+ *                per-tensor scale.  The stem runs in bf16 and quantises its
+ *                output; heads, softmax and value in fp32.
+ *   AZ_FP8_E4M3  as AZ_INT8 with OCP fp8 e4m3 (max 448, saturating, round to
+ *                nearest even) codes and fp32 accumulation.
+ *   For AZ_INT8 / AZ_FP8_E4M3 each output element of residual conv n
+ *   (n = 2j: first conv of block j, n = 2j+1: second) is, in fp32 and in this
+ *   order:  y = float(acc) * (a[n] * s_w[n][f]);  y = y + b[f];
+ *           (second conv only) y = y + float(q_res) * a[n-1];
+ *           q = sat(rne(act(y) * (1 / a[n+1]))).
+ *   The stem output is q = sat(rne(act(float(acc) + b[f]) * (1 / a[0]))) and the
+ *   heads take q * a[2*blocks].
+ *
+ * Threading and streams.  A handle serves one stream at a time: calls on the
+ * same handle from different streams may overlap and must be ordered by the
+ * caller (load one handle per concurrent stream).  Calls on different handles
+ * are independent.  az_last_error() is thread-local.
+ */
+#ifndef AZ_H
+#define AZ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AZ_ABI_VERSION 1
+#define AZ_SQUARES 64
+
+typedef struct az_net az_net; /* opaque: owns the device copy of the packed weights */
+
+typedef enum {
+  AZ_F32 = 0,
+  AZ_BF16 = 1,
+  AZ_INT8 = 2,
+  AZ_FP8_E4M3 = 3
+} az_dtype;
+
+typedef enum {
+  AZ_OK = 0,
+  AZ_ERR_INVALID_ARG = -1, /* NULL pointer, bad size or count, misaligned buffer */
+  AZ_ERR_UNSUPPORTED = -2, /* well-formed spec this build does not implement */
+  AZ_ERR_NOMEM = -3,       /* device allocation failed */
+  AZ_ERR_DEVICE = -4       /* any other HIP runtime failure */
+} az_status;
+
+/* Network shape.  Supported: in_planes 1..32; blocks 1..64; policy_planes
+ * 1..95; value_hidden 1..512; act_cap >= 0 (0 = plain ReLU); max_batch
+ * 1..1048576.  filters: AZ_F32 any multiple of 8 up to 256; AZ_BF16, AZ_INT8
+ * and AZ_FP8_E4M3 one of 64, 128, 256.  Anything else well-formed returns
+ * AZ_ERR_UNSUPPORTED. */
+typedef struct {
+  int32_t abi_version;     /* must be AZ_ABI_VERSION */
+  int32_t in_planes;       /* input planes per position (20 in the synthetic encoding) */
+  int32_t blocks;          /* residual blocks after the stem */
+  int32_t filters;         /* F: channels of the stem and of every block */
+  int32_t policy_planes;   /* P: move-type planes; P*64 policy cells per position */
+  int32_t value_hidden;    /* H: width of the value head's hidden layer */
+  int32_t value_conv_relu; /* 0: no activation after the value 1x1 conv; 1: ReLU */
+  float act_cap;           /* 0: ReLU; > 0: ReLU capped at act_cap */
+  int32_t max_batch;       /* largest B az_eval_batch accepts for this handle */
+} az_layer_spec;
+
+/* Number of floats the canonical weight blob of `spec` must hold, or 0 if the
+ * spec is malformed.  Blob order (fp32, PyTorch layouts, concatenated):
+ *   stem W[F][in_planes][3][3], b[F];
+ *   for each block: W1[F][F][3][3], b1[F], W2[F][F][3][3], b2[F];
+ *   policy W[P][F], b[P]; value conv W[1][F], b[1];
+ *   fc1 W[H][64], b[H]; fc2 W[1][H], b[1]. */
+size_t az_weight_count(const az_layer_spec* spec);
+
+/* Builds a handle on the current HIP device: validates the spec and counts,
+ * rounds (AZ_BF16: nearest even) or quantises (AZ_INT8 / AZ_FP8_E4M3, with the
+ * given scales) the weights, packs them into the kernels' fragment order and
+ * copies them to device memory.  Synchronous.
+ *   weights     host, n_weights floats in blob order; copied, caller keeps ownership.
+ *   w_scales    AZ_INT8 / AZ_FP8_E4M3: host, 2*blocks*F positive finite floats,
+ *               s_w[n][f] for residual conv n; other dtypes: NULL and 0.
+ *   act_scales  AZ_INT8 / AZ_FP8_E4M3: host, 2*blocks+1 positive finite floats,
+ *               a[k] of tensor k in the order h0, t0, h1, t1, ..., h_blocks (h0 is
+ *               the stem output, t_j the first conv's output in block j, h_{j+1}
+ *               block j's output); other dtypes: NULL and 0.
+ *   out         receives the handle; untouched on failure.
+ * Returns AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_UNSUPPORTED, AZ_ERR_NOMEM or
+ * AZ_ERR_DEVICE.  Nothing leaks on failure. */
+int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weights,
+                int32_t dtype, const float* w_scales, size_t n_w_scales,
+                const float* act_scales, size_t n_act_scales, az_net** out);
+
+/* Evaluates B positions, asynchronously on `stream` (a hipStream_t; NULL is the
+ * null stream of the handle's device).  Allocates nothing and never
+ * synchronises, so it can be captured into a HIP graph.
+ *   planes  device, [B][in_planes][8][8] fp32, contiguous, 16-byte aligned.
+ *           AZ_BF16 / AZ_INT8 / AZ_FP8_E4M3 round the planes to bf16 on entry.
+ *   legal   device, [B][P*64] bytes, contiguous, 16-byte aligned; nonzero = legal.
+ *   policy  device, [B][P*64] fp32 out, contiguous, 16-byte aligned; every element
+ *           is written; illegal cells are exactly 0.0f.
+ *   value   device, [B] fp32 out, in [-1, 1].
+ * B == 0 returns AZ_OK and launches nothing.  B < 0, B > max_batch, a NULL or
+ * misaligned pointer return AZ_ERR_INVALID_ARG before touching the device.
+ * Input values are not checked.  Launch failures return AZ_ERR_DEVICE. */
+int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_t B,
+                  float* policy, float* value, void* stream);
+
+/* Kernel tiling used by az_eval_batch.  0: chosen from B (default); 1: four
+ * boards per workgroup (F=64, 128) or two (F=256), for large batches; 2: one
+ * board per workgroup, for small batches.  AZ_F32 has a single tiling and
+ * accepts only 0.  Returns AZ_OK or AZ_ERR_INVALID_ARG. */
+int az_net_set_tiling(az_net* net, int32_t tiling);
+
+/* The tiling az_eval_batch would use for a batch of B (1 or 2; 0 for AZ_F32),
+ * or a negative status. */
+int az_net_tiling_for(const az_net* net, int32_t B);
+
+/* Device bytes held by the handle (packed weights and per-layer constants). */
+size_t az_net_device_bytes(const az_net* net);
+
+/* Frees the handle and its device memory; NULL is a no-op.  The caller must
+ * make sure no evaluation on the handle is still running. */
+void az_net_free(az_net* net);
+
+/* Static description of a status code. */
+const char* az_status_string(int status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* az_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AZ_H */

@@ -1,0 +1,170 @@
+"""ctypes binding of the C ABI in include/az.h (argument marshalling only).
+
+Every computation runs in the HIP library; this module only converts Python
+arguments to the C types and raises on a non-zero status.  It fails loudly if
+the library has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libaz_mi355x.so")
+
+AZ_ABI_VERSION = 1
+AZ_F32, AZ_BF16, AZ_INT8, AZ_FP8_E4M3 = 0, 1, 2, 3
+DTYPES = {"f32": AZ_F32, "bf16": AZ_BF16, "int8": AZ_INT8, "fp8": AZ_FP8_E4M3}
+AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_UNSUPPORTED, AZ_ERR_NOMEM, AZ_ERR_DEVICE = 0, -1, -2, -3, -4
+
+# Every symbol include/az.h declares.
+EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_net_set_tiling",
+           "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_status_string",
+           "az_last_error")
+
+
+class az_layer_spec(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_int32), ("in_planes", ctypes.c_int32),
+                ("blocks", ctypes.c_int32), ("filters", ctypes.c_int32),
+                ("policy_planes", ctypes.c_int32), ("value_hidden", ctypes.c_int32),
+                ("value_conv_relu", ctypes.c_int32), ("act_cap", ctypes.c_float),
+                ("max_batch", ctypes.c_int32)]
+
+
+class AzError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (CDLL); raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2609_37447_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        FP = ctypes.POINTER(ctypes.c_float)
+        L.az_weight_count.argtypes, L.az_weight_count.restype = [ctypes.POINTER(az_layer_spec)], SZ
+        L.az_net_load.argtypes = [ctypes.POINTER(az_layer_spec), FP, SZ, I32, FP, SZ, FP, SZ,
+                                  ctypes.POINTER(P)]
+        L.az_net_load.restype = ctypes.c_int
+        L.az_eval_batch.argtypes = [P, P, P, I32, P, P, P]
+        L.az_eval_batch.restype = ctypes.c_int
+        L.az_net_set_tiling.argtypes, L.az_net_set_tiling.restype = [P, I32], ctypes.c_int
+        L.az_net_tiling_for.argtypes, L.az_net_tiling_for.restype = [P, I32], ctypes.c_int
+        L.az_net_device_bytes.argtypes, L.az_net_device_bytes.restype = [P], SZ
+        L.az_net_free.argtypes, L.az_net_free.restype = [P], None
+        L.az_status_string.argtypes, L.az_status_string.restype = [ctypes.c_int], ctypes.c_char_p
+        L.az_last_error.argtypes, L.az_last_error.restype = [], ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def make_spec(in_planes, blocks, filters, policy_planes, value_hidden, value_conv_relu=0,
+              act_cap=0.0, max_batch=1, abi_version=AZ_ABI_VERSION) -> az_layer_spec:
+    return az_layer_spec(abi_version, in_planes, blocks, filters, policy_planes, value_hidden,
+                         value_conv_relu, act_cap, max_batch)
+
+
+def spec_from_shape(shape, max_batch: int) -> az_layer_spec:
+    """az_layer_spec from any object with the NetShape attribute names."""
+    return make_spec(shape.in_planes, shape.blocks, shape.filters, shape.policy_planes,
+                     shape.value_hidden, shape.value_conv_relu, shape.act_cap, max_batch)
+
+
+def _check(status: int, where: str) -> int:
+    if status < 0:
+        detail = lib().az_last_error().decode(errors="replace")
+        raise AzError(status, where, detail or az_status_string(status))
+    return status
+
+
+def _fptr(a):
+    if a is None:
+        return None, 0
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return a, a.size
+
+
+def az_weight_count(spec: az_layer_spec) -> int:
+    return int(lib().az_weight_count(ctypes.byref(spec)))
+
+
+def az_net_load(spec: az_layer_spec, weights, dtype, w_scales=None, act_scales=None,
+                raise_on_error: bool = True):
+    """Returns the handle (int), or (status) when raise_on_error is False and it fails."""
+    dt = DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+    w, nw = _fptr(weights)
+    ws, nws = _fptr(w_scales)
+    acs, nacs = _fptr(act_scales)
+    FP = ctypes.POINTER(ctypes.c_float)
+    cast = lambda a: a.ctypes.data_as(FP) if a is not None else None  # noqa: E731
+    out = ctypes.c_void_p()
+    st = lib().az_net_load(ctypes.byref(spec), cast(w), nw, dt, cast(ws), nws, cast(acs), nacs,
+                           ctypes.byref(out))
+    if not raise_on_error:
+        return (st, out.value) if st == AZ_OK else (st, None)
+    _check(st, "az_net_load")
+    return out.value
+
+
+def az_eval_batch(net, planes_ptr: int, legal_ptr: int, B: int, policy_ptr: int, value_ptr: int,
+                  stream: int = 0, raise_on_error: bool = True) -> int:
+    st = lib().az_eval_batch(net, planes_ptr, legal_ptr, int(B), policy_ptr, value_ptr, stream)
+    return _check(st, "az_eval_batch") if raise_on_error else st
+
+
+def az_net_set_tiling(net, tiling: int, raise_on_error: bool = True) -> int:
+    st = lib().az_net_set_tiling(net, int(tiling))
+    return _check(st, "az_net_set_tiling") if raise_on_error else st
+
+
+def az_net_tiling_for(net, B: int) -> int:
+    return _check(lib().az_net_tiling_for(net, int(B)), "az_net_tiling_for")
+
+
+def az_net_device_bytes(net) -> int:
+    return int(lib().az_net_device_bytes(net))
+
+
+def az_net_free(net) -> None:
+    lib().az_net_free(net)
+
+
+def az_status_string(status: int) -> str:
+    return lib().az_status_string(int(status)).decode()
+
+
+def az_last_error() -> str:
+    return lib().az_last_error().decode(errors="replace")
+
+
+# --------------------------------------------------------------------------- #
+# torch convenience: device tensors and streams (PyTorch provides memory and
+# streams only)
+# --------------------------------------------------------------------------- #
+def eval_tensors(net, planes, legal, policy, value, stream=None) -> int:
+    """az_eval_batch on torch CUDA tensors; stream defaults to torch's current one."""
+    import torch
+    B = planes.shape[0]
+    for name, t in (("planes", planes), ("legal", legal), ("policy", policy), ("value", value)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous device tensor")
+    if planes.dtype != torch.float32 or legal.dtype != torch.uint8:
+        raise ValueError("planes must be float32 and legal uint8")
+    if policy.dtype != torch.float32 or value.dtype != torch.float32:
+        raise ValueError("policy and value must be float32")
+    if legal.shape[0] != B or policy.shape[0] != B or value.shape[0] != B:
+        raise ValueError("batch sizes differ")
+    s = torch.cuda.current_stream() if stream is None else stream
+    return az_eval_batch(net, planes.data_ptr(), legal.data_ptr(), B, policy.data_ptr(),
+                         value.data_ptr(), s.cuda_stream)

@@ -1,0 +1,45 @@
+// Internal interface between the host runtime (az_runtime.cpp) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+// Rows of the fused policy/value head matrix: policy planes, then the value
+// 1x1 conv row, then zero rows up to three 32-row MFMA blocks.
+#define AZ_HEAD_ROWS 96
+// Largest policy-plane count the fused head supports (one row left for value).
+#define AZ_MAX_POLICY 95
+// Largest input-plane count (the stem pads its channels to 32).
+#define AZ_MAX_IN_PLANES 32
+
+// Device-side description of a loaded network, passed to kernels by value.
+struct AzDevNet {
+  int in_planes, blocks, filters, policy_planes, value_hidden, value_conv_relu;
+  float act_cap;     // +inf when the activation is a plain ReLU
+  float head_scale;  // value of one code of the final tower tensor (1 for float nets)
+  // MFMA dtypes: A-fragment streams (see az_runtime.cpp for the order).
+  // AZ_F32: canonical fp32 arrays.
+  const void* stem_w;
+  const void* tower_w;
+  const void* head_w;
+  const float* bias;    // [(1 + 2*blocks) * F]: stem, then residual conv n = 0..2*blocks-1
+  const float* mscale;  // quantised: [2*blocks*F] a[n] * s_w[n][f]
+  const float* act;     // quantised: [2*blocks+1] tensor scales a[k]
+  const float* inv;     // quantised: [2*blocks+1] 1 / a[k]
+  const float* head_b;  // [AZ_HEAD_ROWS]: policy biases, value conv bias at row P, zeros
+  const float* fc1_w;   // [H][64]
+  const float* fc1_b;   // [H]
+  const float* fc2_w;   // [H]
+  float fc2_b;
+};
+
+// Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small.
+hipError_t az_launch_mfma(int dtype, int tiling, const AzDevNet& net, const float* planes,
+                          const uint8_t* legal, int B, float* policy, float* value,
+                          hipStream_t stream);
+hipError_t az_launch_f32(const AzDevNet& net, const float* planes, const uint8_t* legal, int B,
+                         float* policy, float* value, hipStream_t stream);
+// Boards per workgroup of a tiling (for grid sizing and tests).
+int az_mfma_boards_per_wg(int filters, int tiling);
+// Whether an (dtype, filters) pair has MFMA kernels in this build.
+bool az_mfma_supported(int dtype, int filters);

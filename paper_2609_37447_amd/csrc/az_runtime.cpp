@@ -1,0 +1,397 @@
+// Host side of the C ABI: spec validation, weight rounding / quantisation,
+// packing into the kernels' fragment order, device upload and dispatch.
+//
+// Packed weight streams (MFMA dtypes).  A 3x3 conv with C' input channels
+// (the stem pads 20 -> 32) is the GEMM D[ch][sq] = sum_k W[ch][k] X[k][sq] with
+// k = tap * C' + c, tap = 3*dy + dx.  With KS the reduction length of one MFMA
+// (bf16 16, int8 32, fp8 64) the stream holds, for every K step s and every
+// 32-channel block mb, one 64-lane fragment; lane l carries
+//   W[mb*32 + l%32][s*KS + (KS/2)*(l/32) + t],  t = 0 .. KS/2-1,
+// contiguously (16 bytes for bf16 and int8, 32 for fp8), so that a wave loads
+// a fragment with one fully coalesced read.  The B-operand (activation) lanes
+// use the same k slots, so the pairing of A and B k values matches by
+// construction.  Order: stem (bf16), then the 2*blocks residual convs, then
+// the head: 96 rows (policy planes, value 1x1 conv row, zero rows), K = F.
+#include "../../include/az.h"
+#include "az_internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+#include <vector>
+
+struct az_net {
+  az_layer_spec spec;
+  int dtype;
+  int device;
+  int tiling;  // 0 = chosen per batch
+  void* dmem;
+  size_t dbytes;
+  AzDevNet dn;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  const int st = (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) ? AZ_ERR_NOMEM
+                                                                            : AZ_ERR_DEVICE;
+  return fail(st, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool spec_well_formed(const az_layer_spec* s) {
+  return s && s->abi_version == AZ_ABI_VERSION && s->in_planes >= 1 && s->blocks >= 1 &&
+         s->filters >= 1 && s->policy_planes >= 1 && s->value_hidden >= 1 &&
+         (s->value_conv_relu == 0 || s->value_conv_relu == 1) && s->act_cap >= 0.0f &&
+         isfinite(s->act_cap) && s->max_batch >= 1;
+}
+
+int check_spec(const az_layer_spec* s, int dtype) {
+  if (!spec_well_formed(s)) return fail(AZ_ERR_INVALID_ARG, "malformed az_layer_spec");
+  if (dtype < AZ_F32 || dtype > AZ_FP8_E4M3) return fail(AZ_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+  if (s->in_planes > AZ_MAX_IN_PLANES) return fail(AZ_ERR_UNSUPPORTED, "in_planes %d > %d", s->in_planes, AZ_MAX_IN_PLANES);
+  if (s->blocks > 64) return fail(AZ_ERR_UNSUPPORTED, "blocks %d > 64", s->blocks);
+  if (s->policy_planes > AZ_MAX_POLICY) return fail(AZ_ERR_UNSUPPORTED, "policy_planes %d > %d", s->policy_planes, AZ_MAX_POLICY);
+  if (s->value_hidden > 512) return fail(AZ_ERR_UNSUPPORTED, "value_hidden %d > 512", s->value_hidden);
+  if (s->max_batch > (1 << 20)) return fail(AZ_ERR_UNSUPPORTED, "max_batch %d > 2^20", s->max_batch);
+  if (dtype == AZ_F32) {
+    if (s->filters % 8 != 0 || s->filters > 256) return fail(AZ_ERR_UNSUPPORTED, "AZ_F32 needs filters a multiple of 8 up to 256, got %d", s->filters);
+  } else if (!az_mfma_supported(dtype, s->filters)) {
+    return fail(AZ_ERR_UNSUPPORTED, "dtype %d needs filters in {64, 128, 256}, got %d", dtype, s->filters);
+  }
+  return AZ_OK;
+}
+
+size_t weight_count(const az_layer_spec* s) {
+  const size_t C = s->in_planes, F = s->filters, P = s->policy_planes, H = s->value_hidden;
+  return F * C * 9 + F + (size_t)s->blocks * 2 * (F * F * 9 + F) + P * F + P + F + 1 + H * 64 + H + H + 1;
+}
+
+// Offsets of the arrays inside the canonical blob.
+struct BlobView {
+  const float *stem_w, *stem_b, *pol_w, *pol_b, *val_w, *val_b, *fc1_w, *fc1_b, *fc2_w, *fc2_b;
+  std::vector<const float*> w, b;  // residual conv n = 2j (first) and 2j+1 (second)
+};
+
+BlobView view(const az_layer_spec* s, const float* blob) {
+  const size_t C = s->in_planes, F = s->filters, P = s->policy_planes, H = s->value_hidden;
+  BlobView v;
+  const float* q = blob;
+  v.stem_w = q; q += F * C * 9;
+  v.stem_b = q; q += F;
+  for (int j = 0; j < s->blocks; ++j)
+    for (int k = 0; k < 2; ++k) {
+      v.w.push_back(q); q += F * F * 9;
+      v.b.push_back(q); q += F;
+    }
+  v.pol_w = q; q += P * F;
+  v.pol_b = q; q += P;
+  v.val_w = q; q += F;
+  v.val_b = q; q += 1;
+  v.fc1_w = q; q += H * 64;
+  v.fc1_b = q; q += H;
+  v.fc2_w = q; q += H;
+  v.fc2_b = q; q += 1;
+  return v;
+}
+
+uint16_t bf16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+int8_t quant_i8(float v) {
+  float r = nearbyintf(v);  // default rounding mode: to nearest, ties to even
+  if (r > 127.0f) r = 127.0f;
+  if (r < -127.0f) r = -127.0f;
+  return (int8_t)r;
+}
+
+// OCP fp8 e4m3fn code of v: nearest value, ties to even, saturating to +-448.
+uint8_t quant_e4m3(float v) {
+  const uint8_t sign = signbit(v) ? 0x80 : 0x00;
+  const double a = fabs((double)v);
+  if (!(a > 0.0)) return sign;
+  if (a >= 448.0) return sign | 0x7e;
+  int ex;
+  frexp(a, &ex);  // a = m * 2^ex, m in [0.5, 1)
+  int e = ex - 1;
+  if (e < -6) e = -6;
+  const double step = ldexp(1.0, e - 3);
+  double r = nearbyint(a / step) * step;
+  if (r > 448.0) r = 448.0;
+  if (r == 0.0) return sign;
+  frexp(r, &ex);
+  e = ex - 1;
+  if (e < -6) return sign | (uint8_t)(r / ldexp(1.0, -9));  // subnormal: m * 2^-9
+  const int mant = (int)((r / ldexp(1.0, e) - 1.0) * 8.0);
+  return sign | (uint8_t)(((e + 7) << 3) | mant);
+}
+
+enum Kind { K_BF16 = 0, K_I8 = 1, K_F8 = 2 };
+
+// Packs a 3x3 conv W[F][Cin][3][3] (padded to Cp input channels) into A fragments.
+void pack_conv(const float* W, const float* wscale, int F, int Cin, int Cp, Kind kind,
+               std::vector<uint8_t>& out) {
+  const int KS = kind == K_BF16 ? 16 : kind == K_I8 ? 32 : 64;
+  const int es = kind == K_BF16 ? 2 : 1;
+  const int half = KS / 2, FB = half * es, nMB = F / 32, S = 9 * Cp / KS;
+  const size_t base = out.size();
+  out.resize(base + (size_t)S * nMB * 64 * FB);
+  uint8_t* o = out.data() + base;
+  for (int s = 0; s < S; ++s)
+    for (int mb = 0; mb < nMB; ++mb)
+      for (int l = 0; l < 64; ++l) {
+        const int ch = mb * 32 + l % 32;
+        uint8_t* dst = o + ((size_t)(s * nMB + mb) * 64 + l) * FB;
+        for (int t = 0; t < half; ++t) {
+          const int k = s * KS + half * (l / 32) + t, tap = k / Cp, c = k % Cp;
+          const float v = c < Cin ? W[((size_t)ch * Cin + c) * 9 + tap] : 0.0f;
+          if (kind == K_BF16) {
+            const uint16_t h = bf16_rne(v);
+            memcpy(dst + 2 * t, &h, 2);
+          } else {
+            const float x = v / wscale[ch];  // fp32 division, correctly rounded
+            dst[t] = kind == K_I8 ? (uint8_t)quant_i8(x) : quant_e4m3(x);
+          }
+        }
+      }
+}
+
+void pack_head(const BlobView& v, int F, int P, std::vector<uint8_t>& out) {
+  const int S = F / 16;
+  const size_t base = out.size();
+  out.resize(base + (size_t)S * 3 * 64 * 16);
+  uint8_t* o = out.data() + base;
+  for (int s = 0; s < S; ++s)
+    for (int mb = 0; mb < 3; ++mb)
+      for (int l = 0; l < 64; ++l) {
+        const int row = mb * 32 + l % 32;
+        for (int t = 0; t < 8; ++t) {
+          const int k = s * 16 + 8 * (l / 32) + t;
+          const float w = row < P ? v.pol_w[(size_t)row * F + k] : row == P ? v.val_w[k] : 0.0f;
+          const uint16_t h = bf16_rne(w);
+          memcpy(o + ((size_t)(s * 3 + mb) * 64 + l) * 16 + 2 * t, &h, 2);
+        }
+      }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int choose_tiling(const az_net* n, int B) {
+  if (n->dtype == AZ_F32) return 0;
+  if (n->tiling) return n->tiling;
+  const int bpw = az_mfma_boards_per_wg(n->spec.filters, 1);
+  return (B + bpw - 1) / bpw >= 256 ? 1 : 2;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t az_weight_count(const az_layer_spec* spec) {
+  if (!spec_well_formed(spec)) return 0;
+  return weight_count(spec);
+}
+
+const char* az_status_string(int status) {
+  switch (status) {
+    case AZ_OK: return "ok";
+    case AZ_ERR_INVALID_ARG: return "invalid argument";
+    case AZ_ERR_UNSUPPORTED: return "unsupported network or dtype";
+    case AZ_ERR_NOMEM: return "device out of memory";
+    case AZ_ERR_DEVICE: return "HIP device error";
+    default: return "unknown status";
+  }
+}
+
+const char* az_last_error(void) { return g_err.c_str(); }
+
+int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weights, int32_t dtype,
+                const float* w_scales, size_t n_w_scales, const float* act_scales,
+                size_t n_act_scales, az_net** out) {
+  g_err.clear();
+  if (!out || !weights) return fail(AZ_ERR_INVALID_ARG, "NULL weights or out pointer");
+  int st = check_spec(spec, dtype);
+  if (st != AZ_OK) return st;
+  const az_layer_spec& s = *spec;
+  if (n_weights != weight_count(spec))
+    return fail(AZ_ERR_INVALID_ARG, "n_weights %zu, the spec needs %zu", n_weights, weight_count(spec));
+  const int F = s.filters, NB = s.blocks, P = s.policy_planes, H = s.value_hidden, Cin = s.in_planes;
+  const bool quant = dtype == AZ_INT8 || dtype == AZ_FP8_E4M3;
+  if (quant) {
+    if (!w_scales || n_w_scales != (size_t)2 * NB * F)
+      return fail(AZ_ERR_INVALID_ARG, "need %d weight scales, got %zu", 2 * NB * F, n_w_scales);
+    if (!act_scales || n_act_scales != (size_t)2 * NB + 1)
+      return fail(AZ_ERR_INVALID_ARG, "need %d activation scales, got %zu", 2 * NB + 1, n_act_scales);
+    for (size_t i = 0; i < n_w_scales; ++i)
+      if (!(w_scales[i] > 0.0f) || !isfinite(w_scales[i])) return fail(AZ_ERR_INVALID_ARG, "weight scale %zu not positive finite", i);
+    for (size_t i = 0; i < n_act_scales; ++i)
+      if (!(act_scales[i] > 0.0f) || !isfinite(act_scales[i])) return fail(AZ_ERR_INVALID_ARG, "activation scale %zu not positive finite", i);
+  } else if (w_scales || n_w_scales || act_scales || n_act_scales) {
+    return fail(AZ_ERR_INVALID_ARG, "scales are only taken for AZ_INT8 and AZ_FP8_E4M3");
+  }
+
+  const BlobView v = view(spec, weights);
+  std::vector<uint8_t> stem, tower, head;
+  std::vector<float> bias((size_t)(1 + 2 * NB) * F), mscale, act, inv;
+  std::vector<float> head_b(AZ_HEAD_ROWS, 0.0f), fc2w(v.fc2_w, v.fc2_w + H);
+  memcpy(bias.data(), v.stem_b, F * sizeof(float));
+  for (int n = 0; n < 2 * NB; ++n) memcpy(bias.data() + (size_t)(1 + n) * F, v.b[n], F * sizeof(float));
+  for (int i = 0; i < P; ++i) head_b[i] = v.pol_b[i];
+  head_b[P] = v.val_b[0];
+  try {
+    if (dtype == AZ_F32) {
+      stem.resize((size_t)F * Cin * 9 * 4);
+      memcpy(stem.data(), v.stem_w, stem.size());
+      tower.resize((size_t)2 * NB * F * F * 9 * 4);
+      for (int n = 0; n < 2 * NB; ++n)
+        memcpy(tower.data() + (size_t)n * F * F * 9 * 4, v.w[n], (size_t)F * F * 9 * 4);
+      head.resize((size_t)(P + 1) * F * 4);
+      memcpy(head.data(), v.pol_w, (size_t)P * F * 4);
+      memcpy(head.data() + (size_t)P * F * 4, v.val_w, (size_t)F * 4);
+    } else {
+      pack_conv(v.stem_w, nullptr, F, Cin, 32, K_BF16, stem);
+      const Kind kind = dtype == AZ_BF16 ? K_BF16 : dtype == AZ_INT8 ? K_I8 : K_F8;
+      for (int n = 0; n < 2 * NB; ++n) pack_conv(v.w[n], quant ? w_scales + (size_t)n * F : nullptr, F, F, F, kind, tower);
+      pack_head(v, F, P, head);
+      if (quant) {
+        mscale.resize((size_t)2 * NB * F);
+        for (int n = 0; n < 2 * NB; ++n)
+          for (int f = 0; f < F; ++f) mscale[(size_t)n * F + f] = act_scales[n] * w_scales[(size_t)n * F + f];
+        act.assign(act_scales, act_scales + 2 * NB + 1);
+        inv.resize(2 * NB + 1);
+        for (int k = 0; k < 2 * NB + 1; ++k) inv[k] = (float)(1.0 / (double)act_scales[k]);
+      }
+    }
+  } catch (const std::bad_alloc&) {
+    return fail(AZ_ERR_NOMEM, "host allocation failed while packing weights");
+  }
+
+  // One device allocation, 256-byte aligned sections.
+  struct Sec { const void* src; size_t bytes; size_t off; };
+  std::vector<Sec> secs = {
+      {stem.data(), stem.size(), 0}, {tower.data(), tower.size(), 0}, {head.data(), head.size(), 0},
+      {bias.data(), bias.size() * 4, 0}, {mscale.data(), mscale.size() * 4, 0},
+      {act.data(), act.size() * 4, 0}, {inv.data(), inv.size() * 4, 0},
+      {head_b.data(), head_b.size() * 4, 0}, {v.fc1_w, (size_t)H * 64 * 4, 0},
+      {v.fc1_b, (size_t)H * 4, 0}, {fc2w.data(), fc2w.size() * 4, 0}};
+  size_t total = 0;
+  for (auto& sc : secs) { sc.off = total; total += align256(sc.bytes); }
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  void* dmem = nullptr;
+  e = hipMalloc(&dmem, total);
+  if (e != hipSuccess) { (void)hipGetLastError(); return hip_fail(e, "hipMalloc of the weights"); }
+  for (auto& sc : secs) {
+    if (!sc.bytes) continue;
+    e = hipMemcpy(static_cast<uint8_t*>(dmem) + sc.off, sc.src, sc.bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) { (void)hipFree(dmem); return hip_fail(e, "hipMemcpy of the weights"); }
+  }
+  az_net* net = new (std::nothrow) az_net;
+  if (!net) { (void)hipFree(dmem); return fail(AZ_ERR_NOMEM, "host allocation of the handle failed"); }
+  auto at = [&](int i) { return secs[i].bytes ? static_cast<uint8_t*>(dmem) + secs[i].off : nullptr; };
+  net->spec = s;
+  net->dtype = dtype;
+  net->device = dev;
+  net->tiling = 0;
+  net->dmem = dmem;
+  net->dbytes = total;
+  AzDevNet& d = net->dn;
+  d.in_planes = Cin;
+  d.blocks = NB;
+  d.filters = F;
+  d.policy_planes = P;
+  d.value_hidden = H;
+  d.value_conv_relu = s.value_conv_relu;
+  d.act_cap = s.act_cap > 0.0f ? s.act_cap : INFINITY;
+  d.head_scale = quant ? act_scales[2 * NB] : 1.0f;
+  d.stem_w = at(0);
+  d.tower_w = at(1);
+  d.head_w = at(2);
+  d.bias = reinterpret_cast<const float*>(at(3));
+  d.mscale = reinterpret_cast<const float*>(at(4));
+  d.act = reinterpret_cast<const float*>(at(5));
+  d.inv = reinterpret_cast<const float*>(at(6));
+  d.head_b = reinterpret_cast<const float*>(at(7));
+  d.fc1_w = reinterpret_cast<const float*>(at(8));
+  d.fc1_b = reinterpret_cast<const float*>(at(9));
+  d.fc2_w = reinterpret_cast<const float*>(at(10));
+  d.fc2_b = v.fc2_b[0];
+  *out = net;
+  return AZ_OK;
+}
+
+int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_t B, float* policy,
+                  float* value, void* stream) {
+  if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
+  if (B < 0) return fail(AZ_ERR_INVALID_ARG, "B = %d < 0", B);
+  if (B == 0) return AZ_OK;
+  if (B > net->spec.max_batch) return fail(AZ_ERR_INVALID_ARG, "B = %d > max_batch %d", B, net->spec.max_batch);
+  if (!planes || !legal || !policy || !value) return fail(AZ_ERR_INVALID_ARG, "NULL buffer");
+  if (((uintptr_t)planes | (uintptr_t)legal | (uintptr_t)policy) & 15u)
+    return fail(AZ_ERR_INVALID_ARG, "planes, legal and policy must be 16-byte aligned");
+  if ((uintptr_t)value & 3u) return fail(AZ_ERR_INVALID_ARG, "value must be 4-byte aligned");
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (cur != net->device && (e = hipSetDevice(net->device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (net->dtype == AZ_F32)
+    e = az_launch_f32(net->dn, planes, legal, B, policy, value, s);
+  else
+    e = az_launch_mfma(net->dtype, choose_tiling(net, B), net->dn, planes, legal, B, policy, value, s);
+  if (cur != net->device) (void)hipSetDevice(cur);
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return AZ_OK;
+}
+
+int az_net_set_tiling(az_net* net, int32_t tiling) {
+  if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
+  if (net->dtype == AZ_F32 ? tiling != 0 : (tiling < 0 || tiling > 2))
+    return fail(AZ_ERR_INVALID_ARG, "tiling %d not available for this dtype", tiling);
+  net->tiling = tiling;
+  return AZ_OK;
+}
+
+int az_net_tiling_for(const az_net* net, int32_t B) {
+  if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
+  if (B < 0) return fail(AZ_ERR_INVALID_ARG, "B = %d < 0", B);
+  return choose_tiling(net, B);
+}
+
+size_t az_net_device_bytes(const az_net* net) { return net ? net->dbytes : 0; }
+
+void az_net_free(az_net* net) {
+  if (!net) return;
+  if (net->dmem) {
+    int cur = 0;
+    const bool have = hipGetDevice(&cur) == hipSuccess;
+    if (have && cur != net->device) (void)hipSetDevice(net->device);
+    (void)hipFree(net->dmem);
+    if (have && cur != net->device) (void)hipSetDevice(cur);
+  }
+  delete net;
+}
+
+}  // extern "C"

@@ -1,0 +1,105 @@
+"""Shared helpers for the GPU tests: run the HIP library through the C ABI on
+seeded inputs and compare with the oracle."""
+
+from __future__ import annotations
+
+import functools
+
+import numpy as np
+
+import azgen
+import oracle
+from oracle import az_oracle as O
+
+TOL = {  # max |dP| elementwise, max |dV|
+    "bf16": (1e-2, 2e-2),
+    "int8": (3e-2, 5e-2),
+    "fp8": (3e-2, 5e-2),
+}
+
+
+def gpu_eval(spec_shape, blob, dtype, planes, legal, w_scales=None, act_scales=None, tiling=0,
+             max_batch=None, repeat=1):
+    """Evaluates through az_net_load / az_eval_batch; returns numpy (P, V) (a list of
+    (P, V) when repeat > 1)."""
+    import torch
+
+    import paper_2609_37447_amd as az
+    B = planes.shape[0]
+    spec = az.spec_from_shape(spec_shape, max_batch or max(B, 1))
+    net = az.az_net_load(spec, blob, dtype, w_scales, act_scales)
+    try:
+        if tiling:
+            az.az_net_set_tiling(net, tiling)
+        dev = torch.device("cuda:0")
+        pl = torch.from_numpy(np.ascontiguousarray(planes, dtype=np.float32)).to(dev)
+        lg = torch.from_numpy(np.ascontiguousarray(legal, dtype=np.uint8)).to(dev)
+        outs = []
+        for _ in range(repeat):
+            pol = torch.full((B, legal.shape[1]), float("nan"), device=dev)
+            val = torch.full((B,), float("nan"), device=dev)
+            az.eval_tensors(net, pl, lg, pol, val)
+            torch.cuda.synchronize()
+            outs.append((pol.cpu().numpy().astype(np.float64), val.cpu().numpy().astype(np.float64)))
+    finally:
+        az.az_net_free(net)
+    return outs[0] if repeat == 1 else outs
+
+
+@functools.lru_cache(maxsize=8)
+def quant_scales(wname: str, fmt: str, alpha_fold: bool = True):
+    """(weight scales, activation scales) by absmax calibration on the workload's
+    512 seeded calibration positions, computed by the oracle."""
+    w = azgen.WORKLOADS[wname]
+    blob = azgen.workload_weights(w, alpha_fold)
+    amax = _absmax(wname, alpha_fold)
+    return O.weight_scales(w.shape, blob, fmt), O.act_scales_from_absmax(amax, fmt)
+
+
+@functools.lru_cache(maxsize=8)
+def _absmax(wname: str, alpha_fold: bool):
+    w = azgen.WORKLOADS[wname]
+    blob = azgen.workload_weights(w, alpha_fold)
+    return O.calibrate_absmax(w.shape, blob, azgen.make_calibration_planes(w))
+
+
+def oracle_eval(shape, blob, dtype, planes, legal, w_scales=None, act_scales=None):
+    if dtype in ("f32", "bf16"):
+        return oracle.forward(shape, blob, planes, legal)
+    return oracle.forward_quant(shape, blob, w_scales, act_scales, dtype, planes, legal)
+
+
+def assert_policy_structure(P, legal, atol_sum=1e-5):
+    """Illegal cells exactly 0, legal rows sum to 1, rows without legal cells all zero."""
+    m = legal != 0
+    assert np.all(P[~m] == 0.0), "nonzero prior on an illegal move"
+    assert np.all(np.isfinite(P))
+    has = m.any(axis=1)
+    sums = P.sum(axis=1)
+    assert np.all(np.abs(sums[has] - 1.0) <= atol_sum), np.abs(sums[has] - 1.0).max()
+    assert np.all(sums[~has] == 0.0)
+
+
+def compare(Pg, Vg, Pr, Vr, dtype):
+    tp, tv = TOL[dtype]
+    dp = float(np.abs(Pg - Pr).max())
+    dv = float(np.abs(Vg - Vr).max())
+    assert dp <= tp and dv <= tv, f"{dtype}: max|dP| {dp:.3g} (tol {tp}), max|dV| {dv:.3g} (tol {tv})"
+    return dp, dv
+
+
+def compare_f32(Pg, Vg, Pr, Vr):
+    """fp32 gate: per row max|dP| <= 1e-4 * max P*, |dV| <= 1e-4 * max(|V*|, 1e-2)."""
+    rowmax = Pr.max(axis=1)
+    dp = np.abs(Pg - Pr).max(axis=1)
+    assert np.all(dp <= 1e-4 * rowmax), float((dp / np.maximum(rowmax, 1e-300)).max())
+    dv = np.abs(Vg - Vr)
+    assert np.all(dv <= 1e-4 * np.maximum(np.abs(Vr), 1e-2)), float(dv.max())
+
+
+def top1_agreement(Pa, Pb, legal):
+    m = legal != 0
+    has = m.any(axis=1)
+    a = np.where(m, Pa, -1.0).argmax(axis=1)
+    b = np.where(m, Pb, -1.0).argmax(axis=1)
+    return float(np.mean(a[has] == b[has]))

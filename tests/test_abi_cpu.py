@@ -1,0 +1,104 @@
+"""The C-ABI library loads, exports every symbol include/az.h declares, and turns
+argument errors into status codes before touching a device (no GPU needed)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import azgen
+import paper_2609_37447_amd as az
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "az.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(az_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = az.lib()
+    declared = _header_functions()
+    assert declared, "no declarations parsed"
+    assert set(declared) == set(az.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_weight_count_matches_layer_list():
+    for w in azgen.WORKLOADS.values():
+        spec = az.spec_from_shape(w.shape, w.batch)
+        assert az.az_weight_count(spec) == w.shape.weight_count()
+    assert az.az_weight_count(az.make_spec(20, 20, 128, 73, 128, max_batch=1)) == 5944523
+    assert az.az_weight_count(az.make_spec(20, 2, 32, 73, 64, max_batch=1)) == 49451
+    assert az.az_weight_count(az.make_spec(20, 24, 256, 73, 128, max_batch=1)) == 28397643
+    assert az.az_weight_count(az.make_spec(20, 2, 32, 73, 64, max_batch=1, abi_version=7)) == 0
+    assert az.az_weight_count(az.make_spec(20, 0, 32, 73, 64, max_batch=1)) == 0
+
+
+def test_status_strings():
+    assert az.az_status_string(0) == "ok"
+    for st in (-1, -2, -3, -4):
+        assert az.az_status_string(st) and az.az_status_string(st) != "unknown status"
+    assert az.az_status_string(5) == "unknown status"
+
+
+def _load_status(spec, blob, dtype, ws=None, acs=None):
+    st, h = az.az_net_load(spec, blob, dtype, ws, acs, raise_on_error=False)
+    assert h is None
+    return st
+
+
+def test_load_rejects_bad_arguments_before_device():
+    shape = azgen.WORKLOADS["tiny_2x32_f32_b16"].shape
+    good = az.spec_from_shape(shape, 16)
+    blob = np.zeros(shape.weight_count(), dtype=np.float32)
+    # wrong weight count
+    assert _load_status(good, blob[:-1], "f32") == az.AZ_ERR_INVALID_ARG
+    assert "n_weights" in az.az_last_error()
+    # malformed spec
+    for bad in (az.make_spec(20, 2, 32, 73, 64, max_batch=0),
+                az.make_spec(20, 2, 32, 73, 64, max_batch=4, abi_version=2),
+                az.make_spec(20, 2, 32, 73, 64, value_conv_relu=3, max_batch=4),
+                az.make_spec(20, 2, 32, 73, 64, act_cap=-1.0, max_batch=4)):
+        assert _load_status(bad, blob, "f32") == az.AZ_ERR_INVALID_ARG
+    # unknown dtype
+    assert _load_status(good, blob, 9) == az.AZ_ERR_INVALID_ARG
+    # unsupported shapes
+    assert _load_status(good, blob, "bf16") == az.AZ_ERR_UNSUPPORTED          # F=32 on MFMA
+    sp = az.make_spec(40, 2, 32, 73, 64, max_batch=4)
+    assert _load_status(sp, np.zeros(az.az_weight_count(sp), np.float32), "f32") == az.AZ_ERR_UNSUPPORTED
+    sp = az.make_spec(20, 2, 32, 96, 64, max_batch=4)
+    assert _load_status(sp, np.zeros(az.az_weight_count(sp), np.float32), "f32") == az.AZ_ERR_UNSUPPORTED
+    sp = az.make_spec(20, 2, 36, 73, 64, max_batch=4)
+    assert _load_status(sp, np.zeros(az.az_weight_count(sp), np.float32), "f32") == az.AZ_ERR_UNSUPPORTED
+    # scales: missing for quantised dtypes, present for float ones, wrong counts, non-positive
+    shp = azgen.WORKLOADS["net20x128_int8_b1024"].shape
+    sp = az.spec_from_shape(shp, 8)
+    b2 = np.zeros(shp.weight_count(), np.float32)
+    ws = np.ones(2 * shp.blocks * shp.filters, np.float32)
+    acs = np.ones(2 * shp.blocks + 1, np.float32)
+    assert _load_status(sp, b2, "int8") == az.AZ_ERR_INVALID_ARG
+    assert _load_status(sp, b2, "int8", ws[:-1], acs) == az.AZ_ERR_INVALID_ARG
+    assert _load_status(sp, b2, "fp8", ws, acs[:-1]) == az.AZ_ERR_INVALID_ARG
+    assert _load_status(sp, b2, "bf16", ws, acs) == az.AZ_ERR_INVALID_ARG
+    bad = ws.copy()
+    bad[3] = 0.0
+    assert _load_status(sp, b2, "int8", bad, acs) == az.AZ_ERR_INVALID_ARG
+    bad = acs.copy()
+    bad[0] = np.nan
+    assert _load_status(sp, b2, "fp8", ws, bad) == az.AZ_ERR_INVALID_ARG
+
+
+def test_eval_and_free_reject_null_handle():
+    assert az.az_eval_batch(None, 0, 0, 4, 0, 0, 0, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
+    assert az.az_net_set_tiling(None, 1, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
+    assert az.az_net_device_bytes(None) == 0
+    az.az_net_free(None)                                     # no-op
+    with pytest.raises(az.AzError):
+        az.az_eval_batch(None, 0, 0, 4, 0, 0, 0)

