@@ -101,7 +101,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="net20x128_int8_b1024", choices=sorted(azgen.WORKLOADS))
-    ap.add_argument("--tiling", type=int, default=0, choices=(0, 1, 2))
+    ap.add_argument("--tiling", type=int, default=0, choices=(0, 1, 2, 3))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     args = ap.parse_args()

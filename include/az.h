@@ -38,14 +38,24 @@
  *                per-tensor scale.  The stem runs in bf16 and quantises its
  *                output; heads, softmax and value in fp32.
  *   AZ_FP8_E4M3  as AZ_INT8 with OCP fp8 e4m3 (max 448, saturating, round to
- *                nearest even) codes and fp32 accumulation.
- *   For AZ_INT8 / AZ_FP8_E4M3 each output element of residual conv n
- *   (n = 2j: first conv of block j, n = 2j+1: second) is, in fp32 and in this
- *   order:  y = float(acc) * (a[n] * s_w[n][f]);  y = y + b[f];
- *           (second conv only) y = y + float(q_res) * a[n-1];
- *           q = sat(rne(act(y) * (1 / a[n+1]))).
- *   The stem output is q = sat(rne(act(float(acc) + b[f]) * (1 / a[0]))) and the
- *   heads take q * a[2*blocks].
+ *                nearest even) codes and fp32 accumulation.  The matrix cores
+ *                sum each run of 8 consecutive input channels of one tap with
+ *                every product truncated toward zero to 2^(E-13), E the largest
+ *                exponent among that run's nonzero products, and add each run's
+ *                sum to the fp32 accumulator rounding to nearest even.
+ *   Heads (1x1 policy and value convolutions) use bf16-rounded weights with fp32
+ *   accumulation under every dtype except AZ_F32.
+ *   For AZ_INT8 / AZ_FP8_E4M3, with inv[k] = float(1 / a[k]) and
+ *   qhi[k] = min(qmax, act_cap * inv[k]) (qmax when act_cap is 0), each output
+ *   element of residual conv n (n = 2j: first conv of block j, n = 2j+1:
+ *   second) writing tensor k = n+1 is, in fp32 with single roundings:
+ *           z = fma(float(acc), (a[n] * s_w[n][f]) * inv[k], b[f] * inv[k]);
+ *           (second conv only) z = fma(float(q_res), a[k-2] * inv[k], z);
+ *           q = round_to_code(min(max(z, 0), qhi[k]))
+ *   where q_res is the code of tensor k-2 (the block's input) and round_to_code
+ *   rounds to nearest even (an integer for int8, an e4m3 value for fp8).  The
+ *   stem writes q = round_to_code(min(max(fma(acc, inv[0], b[f] * inv[0]), 0),
+ *   qhi[0])) from its bf16 accumulation, and the heads take q * a[2*blocks].
  *
  * Threading and streams.  A handle serves one stream at a time: calls on the
  * same handle from different streams may overlap and must be ordered by the
@@ -140,14 +150,17 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
 int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_t B,
                   float* policy, float* value, void* stream);
 
-/* Kernel tiling used by az_eval_batch.  0: chosen from B (default); 1: four
- * boards per workgroup (F=64, 128) or two (F=256), for large batches; 2: one
- * board per workgroup, for small batches.  AZ_F32 has a single tiling and
- * accepts only 0.  Returns AZ_OK or AZ_ERR_INVALID_ARG. */
+/* Kernel tiling used by az_eval_batch.  0: chosen from B and the dtype
+ * (default); 1 (large): four boards per workgroup (F = 64, 128) or two
+ * (F = 256), one workgroup per compute unit; 2 (small): one board per
+ * workgroup; 3 (medium, F = 64 and 128 only): two boards per workgroup, two
+ * workgroups per compute unit.  Every tiling computes bitwise the same
+ * results.  AZ_F32 has a single tiling and accepts only 0.  Returns AZ_OK or
+ * AZ_ERR_INVALID_ARG. */
 int az_net_set_tiling(az_net* net, int32_t tiling);
 
-/* The tiling az_eval_batch would use for a batch of B (1 or 2; 0 for AZ_F32),
- * or a negative status. */
+/* The tiling az_eval_batch would use for a batch of B (1, 2 or 3; 0 for
+ * AZ_F32), or a negative status. */
 int az_net_tiling_for(const az_net* net, int32_t B);
 
 /* Device bytes held by the handle (packed weights and per-layer constants). */

@@ -22,10 +22,19 @@ struct AzDevNet {
   const void* stem_w;
   const void* tower_w;
   const void* head_w;
-  const float* bias;    // [(1 + 2*blocks) * F]: stem, then residual conv n = 0..2*blocks-1
-  const float* mscale;  // quantised: [2*blocks*F] a[n] * s_w[n][f]
-  const float* act;     // quantised: [2*blocks+1] tensor scales a[k]
-  const float* inv;     // quantised: [2*blocks+1] 1 / a[k]
+  // Per-channel epilogue constants, [(1 + 2*blocks) * F]: the stem, then residual
+  // conv n = 0..2*blocks-1.  Float nets: bias = b.  Quantised nets: the
+  // requantising multiply-add z = fma(acc, qmul, bias) with
+  //   stem:   qmul = 1/a[0],                       bias = b * (1/a[0])
+  //   conv n: qmul = (a[n] * s_w[n][f]) * (1/a[n+1]), bias = b * (1/a[n+1])
+  const float* bias;
+  const float* qmul;
+  // Quantised nets, per output tensor k = 0..2*blocks (tensor k is written by
+  // conv k-1, the stem for k = 0): qres[k] = a[k-2] / a[k] for the second conv
+  // of a block (its residual input h scaled into the output's code units),
+  // qhi[k] = min(qmax, act_cap / a[k]) (activation cap and saturation).
+  const float* qres;
+  const float* qhi;
   const float* head_b;  // [AZ_HEAD_ROWS]: policy biases, value conv bias at row P, zeros
   const float* fc1_w;   // [H][64]
   const float* fc1_b;   // [H]
@@ -33,7 +42,7 @@ struct AzDevNet {
   float fc2_b;
 };
 
-// Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small.
+// Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small, 3 = medium.
 hipError_t az_launch_mfma(int dtype, int tiling, const AzDevNet& net, const float* planes,
                           const uint8_t* legal, int B, float* policy, float* value,
                           hipStream_t stream);
@@ -41,5 +50,7 @@ hipError_t az_launch_f32(const AzDevNet& net, const float* planes, const uint8_t
                          float* policy, float* value, hipStream_t stream);
 // Boards per workgroup of a tiling (for grid sizing and tests).
 int az_mfma_boards_per_wg(int filters, int tiling);
+// Whether a tiling id (1 large, 2 small, 3 medium) exists for a filter count.
+bool az_mfma_tiling_valid(int filters, int tiling);
 // Whether an (dtype, filters) pair has MFMA kernels in this build.
 bool az_mfma_supported(int dtype, int filters);

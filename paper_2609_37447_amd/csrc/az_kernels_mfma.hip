@@ -16,10 +16,24 @@
 // no im2col is materialised; a shifted window is just a different LDS row per
 // lane, and out-of-board taps read a zero row.
 //
+// The K loop runs over the nine taps; each tap's K steps are unrolled with
+// compile-time register indices, so accumulators stay in the accumulation
+// registers, weight fragments are double-buffered one prefetch group ahead
+// (crossing taps and layers), and the LDS fragments of step k+1 are read while
+// the MFMAs of step k run.  The epilogue (bias, residual, activation,
+// requantisation) runs once per layer, followed by one workgroup barrier; its
+// per-channel constants are staged through LDS one layer ahead.
+//
 // Activation layout in LDS: [board][square][channel], one row of F channels
 // per square, stored in 16-byte chunks whose position is XOR-swizzled by the
 // square index so that the 16 lanes of a ds_read_b128 group (16 consecutive
 // squares, same logical chunk) hit 16 different bank groups.
+//
+// bf16 networks keep the residual stream (every block input h) in fp32 in the
+// registers of the wave that produces it: each wave owns the same output tile
+// in every layer, so the residual of an output element lives in the lane that
+// computes it.  LDS holds bf16(h), the convolution operand.  The heads read h
+// as bf16(h) + bf16(h - bf16(h)).
 //
 // MFMA output layout (32x32 blocks): lane l holds column l%32 and rows
 // 8*(v/4) + 4*(l/32) + v%4 of its 16 accumulators v, i.e. four runs of four
@@ -28,6 +42,8 @@
 #include "az_internal.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace {
 
@@ -71,6 +87,20 @@ template <> struct Mk<MK_F8> {
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+template <int I, class T>
+__device__ __forceinline__ T& pick(T& a, T& b) {
+  if constexpr (I == 0) return a;
+  else return b;
+}
+
 // Chunk swizzle for a row of RB bytes: rows of 256 bytes or more XOR with the
 // low four square bits; shorter rows first spread consecutive squares over the
 // bank groups a 256-byte line offers.
@@ -106,31 +136,35 @@ __device__ __forceinline__ uint32_t bf16_bits(float f) {
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return bf16_bits(a) | (bf16_bits(b) << 16);
 }
-__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
+__device__ __forceinline__ float bf16_round(float f) { return __uint_as_float(bf16_bits(f) << 16); }
 
 __device__ __forceinline__ float act_fn(float y, float cap) { return fminf(fmaxf(y, 0.0f), cap); }
+__device__ __forceinline__ float med3(float x, float lo, float hi) {
+  return __builtin_amdgcn_fmed3f(x, lo, hi);
+}
 
-__device__ __forceinline__ uint32_t q_i8(float v) {
-  v = fminf(fmaxf(rintf(v), -127.0f), 127.0f);
-  return (uint32_t)((int)v) & 0xffu;
+// Codes of four requantised values already clamped to [0, hi] (hi <= qmax).
+// Both hardware conversions round to nearest even (int8: float -> u8 with the
+// default rounding mode; the values are non-negative and at most 127).
+template <int MK>
+__device__ __forceinline__ uint32_t pack_codes(float z0, float z1, float z2, float z3) {
+  if constexpr (MK == MK_I8) {
+    uint32_t w = __builtin_amdgcn_cvt_pk_u8_f32(z0, 0, 0u);
+    w = __builtin_amdgcn_cvt_pk_u8_f32(z1, 1, w);
+    w = __builtin_amdgcn_cvt_pk_u8_f32(z2, 2, w);
+    return __builtin_amdgcn_cvt_pk_u8_f32(z3, 3, w);
+  } else {
+    int w = __builtin_amdgcn_cvt_pk_fp8_f32(z0, z1, 0, false);
+    w = __builtin_amdgcn_cvt_pk_fp8_f32(z2, z3, w, true);
+    return (uint32_t)w;
+  }
 }
-__device__ __forceinline__ uint32_t pack_q4(int mk, float y0, float y1, float y2, float y3) {
-  if (mk == MK_I8) return q_i8(y0) | (q_i8(y1) << 8) | (q_i8(y2) << 16) | (q_i8(y3) << 24);
-  // The hardware conversion rounds to nearest even but turns |x| > 448 into
-  // NaN, so saturate first.
-  y0 = fminf(fmaxf(y0, -448.0f), 448.0f);
-  y1 = fminf(fmaxf(y1, -448.0f), 448.0f);
-  y2 = fminf(fmaxf(y2, -448.0f), 448.0f);
-  y3 = fminf(fmaxf(y3, -448.0f), 448.0f);
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, 0, false);
-  w = __builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, w, true);
-  return (uint32_t)w;
-}
-template <int R>
-__device__ __forceinline__ float dq_code(int mk, uint32_t x) {
-  if (mk == MK_I8) return (float)(int)(int8_t)(x >> (8 * R));
-  return __builtin_amdgcn_cvt_f32_fp8((int)x, R);
+// Value of byte R of a code word (codes of post-activation tensors are >= 0
+// for int8; fp8 codes are decoded by the hardware conversion).
+template <int MK, int R>
+__device__ __forceinline__ float code_value(uint32_t x) {
+  if constexpr (MK == MK_I8) return (float)(int)(int8_t)(x >> (8 * R));
+  else return __builtin_amdgcn_cvt_f32_fp8((int)x, R);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -142,59 +176,66 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Per-tap LDS row addresses of the wave's N-blocks (square = half a board).
-template <int RB_IN, int NBW>
-__device__ __forceinline__ void tap_rows(int tap, int in_off, int zero_off, int nb0, int l32,
-                                         int (&row)[NBW], int (&sw)[NBW]) {
+// LDS row address and swizzle of lane square j of half-board block nb for a tap.
+// A tap outside the board reads the all-zero region instead, at the bank slot
+// its (virtual) square r*8 + c would occupy: the slots a shifted window leaves
+// free, so the 16 lanes of a read group never collide.
+template <int RB_IN>
+__device__ __forceinline__ void tap_row(int tap, int in_off, int zero_off, int nb, int l32, int& row,
+                                        int& sw) {
   const int dy = tap / 3 - 1, dx = tap % 3 - 1;
-#pragma unroll
-  for (int i = 0; i < NBW; ++i) {
-    const int nb = nb0 + i, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
-    const int r = (j >> 3) + dy, c = (j & 7) + dx;
-    const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
-    const int src = r * 8 + c;
-    row[i] = ok ? in_off + (bl * 64 + src) * RB_IN : zero_off;
-    sw[i] = ok ? swz<RB_IN>(src) : 0;
-  }
+  const int bl = nb >> 1, j = ((nb & 1) << 5) + l32;
+  const int r = (j >> 3) + dy, c = (j & 7) + dx;
+  const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
+  const int src = r * 8 + c;
+  row = ok ? in_off + (bl * 64 + src) * RB_IN : zero_off + ((src * RB_IN) & 255);
+  sw = swz<RB_IN>(src);
 }
 
 // Tile shape: the wave owns MBW 32-channel blocks x NBW 32-square blocks; the
-// workgroup is WM x WN waves; G consecutive K steps form one prefetch group.
-template <int MK, int F, int MBW, int NBW, int WM, int WN, int G>
+// workgroup is WM x WN waves; G consecutive K steps form one weight prefetch
+// group; OCC workgroups share a compute unit.
+template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC>
 struct Cfg {
   using T = Mk<MK>;
   static constexpr int NW = WM * WN, NT = 64 * NW;
   static constexpr int BPW = NBW * WN / 2;  // boards per workgroup
   static constexpr int NMB = F / 32;
   static_assert(NMB == MBW * WM, "channel tiling");
-  static_assert(NBW % 2 == 0 || WN == 1, "board tiling");
+  static_assert(NBW % 2 == 0, "board tiling");
   static constexpr int RB = F * T::ES;  // bytes per square row, tower tensors
   static constexpr int BUF = BPW * 64 * RB;
   static constexpr int OFF_H = 0, OFF_T = BUF, OFF_Z = 2 * BUF;
-  static constexpr int ZB = cmax(RB, 64);
+  static constexpr int ZB = cmax(RB, 256);  // zero region: a 256-byte bank window at least
   static constexpr int RBX = 2 * F;  // bf16 row bytes of the heads' input
-  static constexpr int OFF_X = MK == MK_BF16 ? OFF_H : OFF_T;
+  static constexpr int OFF_X = OFF_T;
   static constexpr int LBMAX = (AZ_MAX_POLICY + 1) * 64;  // floats per board, logits + u
+  // per-layer epilogue constants, double-buffered: [2 slots][bias F | qmul F] floats
+  static constexpr int OFF_K = 2 * BUF + ZB;
+  static constexpr int KSLOT = 2 * F * 4;
   static constexpr int SMEM =
-      cmax(cmax(2 * BUF + ZB, OFF_X + BPW * 64 * RBX), BPW * LBMAX * 4);
-  static_assert(SMEM <= 160 * 1024, "LDS");
+      cmax(cmax(OFF_K + 2 * KSLOT, OFF_X + BPW * 64 * RBX), BPW * LBMAX * 4);
+  static_assert(SMEM * OCC <= 160 * 1024, "LDS");
   static constexpr int CPT = F / T::KS;  // K steps per tap
   static_assert(CPT % G == 0, "group size");
-  static constexpr int GPT = CPT / G, GPL = 9 * GPT;
+  static constexpr int S = 9 * CPT;      // K steps per layer
+  static constexpr int GPL = S / G;      // prefetch groups per layer
   static constexpr int STEP_BYTES = NMB * 64 * T::FB;
-  static constexpr size_t LAYER_BYTES = (size_t)9 * CPT * STEP_BYTES;
+  static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
   static constexpr int NBH = (2 * BPW + NW - 1) / NW;  // head N-blocks per wave
 };
 
-template <int MK, int F, int MBW, int NBW, int WM, int WN, int G>
-__global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
-    AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal, int B,
-    float* __restrict__ policy, float* __restrict__ value) {
-  using C = Cfg<MK, F, MBW, NBW, WM, WN, G>;
+template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
+                          amdgpu_waves_per_eu(OCC, OCC))) void
+az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal, int B,
+              float* __restrict__ policy, float* __restrict__ value) {
+  using C = Cfg<MK, F, MBW, NBW, WM, WN, G, OCC>;
   using T = typename C::T;
   using SB = Mk<MK_BF16>;
   using frag_t = typename T::frag;
   using acc_t = typename T::acc;
+  constexpr bool QUANT = MK != MK_BF16;
   constexpr int NW = C::NW, NT = C::NT, BPW = C::BPW, NMB = C::NMB, RB = C::RB;
   constexpr int OFF_H = C::OFF_H, OFF_T = C::OFF_T, OFF_Z = C::OFF_Z;
 
@@ -209,22 +250,48 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
   const int Cin = p.in_planes;
   const float cap = p.act_cap;
 
+  // fp32 residual stream of the wave's output tile (bf16 networks)
+  float res[QUANT ? 1 : MBW][QUANT ? 1 : NBW][16];
+
   // ---- ingest: zero row, planes -> bf16 [board][square][32 channels] at OFF_T
   for (int i = tid; i < C::ZB / 16; i += NT)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
-  for (int idx = tid; idx < BPW * 256; idx += NT) {
-    const int sq = idx & 63, ck = (idx >> 6) & 3, bl = idx >> 8, b = b0 + bl;
-    uint32_t pk[4];
+  // one item = 4 squares of one (board, input plane): a 16-byte load, four bf16 stores
+  for (int idx = tid; idx < BPW * 32 * 16; idx += NT) {
+    const int q4 = idx & 15, c = (idx >> 4) & 31, bl = idx >> 9, b = b0 + bl;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (b < B && c < Cin) v = *reinterpret_cast<const float4*>(planes + ((size_t)b * Cin + c) * 64 + q4 * 4);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int t = 0; t < 8; t += 2) {
-      const int c = ck * 8 + t;
-      const float v0 = (b < B && c < Cin) ? planes[((size_t)b * Cin + c) * 64 + sq] : 0.0f;
-      const float v1 = (b < B && c + 1 < Cin) ? planes[((size_t)b * Cin + c + 1) * 64 + sq] : 0.0f;
-      pk[t / 2] = pack_bf16x2(v0, v1);
+    for (int r = 0; r < 4; ++r) {
+      const int sq = q4 * 4 + r;
+      *reinterpret_cast<unsigned short*>(smem + OFF_T + (bl * 64 + sq) * 64 + (((c >> 3) ^ swz<64>(sq)) << 4) +
+                                         (c & 7) * 2) = (unsigned short)bf16_bits(vv[r]);
     }
-    *reinterpret_cast<i32x4*>(smem + OFF_T + (bl * 64 + sq) * 64 + ((ck ^ swz<64>(sq)) << 4)) =
-        i32x4{(int)pk[0], (int)pk[1], (int)pk[2], (int)pk[3]};
   }
+
+  // first weight group of the tower, in flight during the stem
+  const uint8_t* tw = static_cast<const uint8_t*>(p.tower_w) + (size_t)(mb0 * 64 + lane) * T::FB;
+  frag_t A0[G][MBW], A1[G][MBW];
+  auto load_group = [&](frag_t(&dst)[G][MBW], const uint8_t* src) {
+#pragma unroll
+    for (int s = 0; s < G; ++s)
+#pragma unroll
+      for (int m = 0; m < MBW; ++m) dst[s][m] = g_frag<MK>(src + s * C::STEP_BYTES + m * 64 * T::FB);
+  };
+  load_group(A0, tw);
+  // per-layer epilogue constants: thread t < F/2 carries float4 t of [bias | qmul]
+  auto load_consts = [&](int k) -> float4 {  // k = 1 + conv index (0 = stem)
+    if (tid < F / 4) return *reinterpret_cast<const float4*>(p.bias + (size_t)k * F + tid * 4);
+    if (QUANT && tid < F / 2) return *reinterpret_cast<const float4*>(p.qmul + (size_t)k * F + (tid - F / 4) * 4);
+    return make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  auto store_consts = [&](int slot, const float4& v) {
+    if (tid < (QUANT ? F / 2 : F / 4))
+      *reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT + tid * 16) = v;
+  };
+  static_assert(NT >= F / 2, "constant staging needs F/2 threads");
+  store_consts(0, load_consts(1));
   __syncthreads();
 
   // ---- stem: bf16 3x3 conv over 32 (padded) input channels, K = 288
@@ -232,16 +299,18 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
     constexpr int SSTEP = NMB * 64 * 16;
     const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)(mb0 * 64 + lane) * 16;
     f32x16 sacc[MBW][NBW];
-#pragma unroll
-    for (int m = 0; m < MBW; ++m)
-#pragma unroll
-      for (int n = 0; n < NBW; ++n) sacc[m][n] = f32x16{};
     SB::frag a[2][2][MBW];
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int m = 0; m < MBW; ++m) a[0][s][m] = g_frag<MK_BF16>(sw8 + s * SSTEP + m * 64 * 16);
-    int row[NBW], sw[NBW];
+    int row[NBW], sw[NBW], nrow[NBW], nsw[NBW];
+    SB::frag bc[NBW], bn[NBW];
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) {
+      tap_row<64>(0, OFF_T, OFF_Z, nb0 + n, l32, row[n], sw[n]);
+      bc[n] = lds_frag<MK_BF16>(smem, row[n], sw[n], lhi);
+    }
 #pragma unroll
     for (int tap = 0; tap < 9; ++tap) {
       if (tap + 1 < 9) {
@@ -249,166 +318,228 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
         for (int s = 0; s < 2; ++s)
 #pragma unroll
           for (int m = 0; m < MBW; ++m)
-            a[(tap + 1) & 1][s][m] =
-                g_frag<MK_BF16>(sw8 + ((tap + 1) * 2 + s) * SSTEP + m * 64 * 16);
+            a[(tap + 1) & 1][s][m] = g_frag<MK_BF16>(sw8 + ((tap + 1) * 2 + s) * SSTEP + m * 64 * 16);
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) tap_row<64>(tap + 1, OFF_T, OFF_Z, nb0 + n, l32, nrow[n], nsw[n]);
       }
-      tap_rows<64, NBW>(tap, OFF_T, OFF_Z, nb0, l32, row, sw);
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        SB::frag bfr[NBW];
+        if (s == 0) {
 #pragma unroll
-        for (int n = 0; n < NBW; ++n) bfr[n] = lds_frag<MK_BF16>(smem, row[n], sw[n], 2 * s + lhi);
+          for (int n = 0; n < NBW; ++n) bn[n] = lds_frag<MK_BF16>(smem, row[n], sw[n], 2 + lhi);
+        } else if (tap + 1 < 9) {
+#pragma unroll
+          for (int n = 0; n < NBW; ++n) bn[n] = lds_frag<MK_BF16>(smem, nrow[n], nsw[n], lhi);
+        }
 #pragma unroll
         for (int m = 0; m < MBW; ++m)
 #pragma unroll
-          for (int n = 0; n < NBW; ++n) sacc[m][n] = SB::mma(a[tap & 1][s][m], bfr[n], sacc[m][n]);
+          for (int n = 0; n < NBW; ++n)
+            sacc[m][n] = SB::mma(a[tap & 1][s][m], bc[n], (tap == 0 && s == 0) ? f32x16{} : sacc[m][n]);
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
+      }
+      if (tap + 1 < 9) {
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) {
+          row[n] = nrow[n];
+          sw[n] = nsw[n];
+        }
       }
     }
     // epilogue: bias, activation, store in the tower format at OFF_H
-    {
-#pragma clang fp contract(off)
-      const float inv0 = MK == MK_BF16 ? 1.0f : p.inv[0];
-#pragma unroll
-      for (int m = 0; m < MBW; ++m)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
-          const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
-#pragma unroll
-          for (int n = 0; n < NBW; ++n) {
-            const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
-            const f32x16& v = sacc[m][n];
-            const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
-            const float y2 = act_fn(v[4 * q + 2] + bb.z, cap), y3 = act_fn(v[4 * q + 3] + bb.w, cap);
-            const int rowo = OFF_H + (bl * 64 + j) * RB;
-            if constexpr (MK == MK_BF16) {
-              *reinterpret_cast<uint2*>(smem + rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi) =
-                  make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
-            } else {
-              *reinterpret_cast<uint32_t*>(smem + rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15)) =
-                  pack_q4(MK, y0 * inv0, y1 * inv0, y2 * inv0, y3 * inv0);
-            }
-          }
-        }
-    }
-  }
-  __syncthreads();
-
-  // ---- residual tower: 2*blocks convolutions, H -> T -> H ...
-  {
-    constexpr int GPL = C::GPL, GPT = C::GPT;
-    const int NG = 2 * p.blocks * GPL;
-    const uint8_t* tw = static_cast<const uint8_t*>(p.tower_w) + (size_t)(mb0 * 64 + lane) * T::FB;
-    frag_t A0[G][MBW], A1[G][MBW];
-    acc_t c[MBW][NBW];
 #pragma unroll
     for (int m = 0; m < MBW; ++m)
 #pragma unroll
-      for (int n = 0; n < NBW; ++n) c[m][n] = acc_t{};
-    int row[NBW], sw[NBW];
-
-    auto load = [&](frag_t(&dst)[G][MBW], int g) {
-      const int layer = g / GPL, gi = g - layer * GPL;
-      const uint8_t* src = tw + layer * C::LAYER_BYTES + (size_t)gi * G * C::STEP_BYTES;
+      for (int q = 0; q < 4; ++q) {
+        const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
+        const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
+        float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
+        if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
 #pragma unroll
-      for (int s = 0; s < G; ++s)
-#pragma unroll
-        for (int m = 0; m < MBW; ++m) dst[s][m] = g_frag<MK>(src + s * C::STEP_BYTES + m * 64 * T::FB);
-    };
+        for (int n = 0; n < NBW; ++n) {
+          const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
+          const f32x16& v = sacc[m][n];
+          const int rowo = OFF_H + (bl * 64 + j) * RB;
+          if constexpr (!QUANT) {
+            const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
+            const float y2 = act_fn(v[4 * q + 2] + bb.z, cap), y3 = act_fn(v[4 * q + 3] + bb.w, cap);
+            res[m][n][4 * q + 0] = y0;
+            res[m][n][4 * q + 1] = y1;
+            res[m][n][4 * q + 2] = y2;
+            res[m][n][4 * q + 3] = y3;
+            *reinterpret_cast<uint2*>(smem + rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi) =
+                make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+          } else {
+            const float hi = p.qhi[0];
+            const float z0 = med3(__builtin_fmaf(v[4 * q + 0], mm.x, bb.x), 0.0f, hi);
+            const float z1 = med3(__builtin_fmaf(v[4 * q + 1], mm.y, bb.y), 0.0f, hi);
+            const float z2 = med3(__builtin_fmaf(v[4 * q + 2], mm.z, bb.z), 0.0f, hi);
+            const float z3 = med3(__builtin_fmaf(v[4 * q + 3], mm.w, bb.w), 0.0f, hi);
+            *reinterpret_cast<uint32_t*>(smem + rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15)) =
+                pack_codes<MK>(z0, z1, z2, z3);
+          }
+        }
+      }
+  }
+  __syncthreads();
 
-    auto epilogue = [&](int n_conv) {
-#pragma clang fp contract(off)
-      const bool second = n_conv & 1;
-      const int out_off = second ? OFF_H : OFF_T;
-      const float* bias = p.bias + (size_t)(1 + n_conv) * F;
-      float inv_out = 1.0f, a_res = 0.0f;
-      const float* ms = nullptr;
-      if constexpr (MK != MK_BF16) {
-        inv_out = p.inv[n_conv + 1];
-        a_res = second ? p.act[n_conv - 1] : 0.0f;
-        ms = p.mscale + (size_t)n_conv * F;
+  // ---- residual tower: per block conv1 (H -> T) and conv2 (T -> H, + residual)
+  {
+    constexpr int CPT = C::CPT, GPL = C::GPL, GPT = CPT / G;
+    acc_t c[MBW][NBW];
+    const int nconv = 2 * p.blocks;
+
+    auto conv = [&](auto second_c, auto par_c, int n_conv) {
+      constexpr bool SECOND = decltype(second_c)::value;
+      constexpr int PAR = decltype(par_c)::value;
+      const uint8_t* wl = tw + (size_t)n_conv * C::LAYER_BYTES;
+      const bool has_next = n_conv + 1 < nconv;
+      const int in_off = SECOND ? OFF_T : OFF_H;
+      const int out_off = SECOND ? OFF_H : OFF_T;
+      // the next layer's epilogue constants, parked in LDS before this layer's barrier
+      const float4 kn = has_next ? load_consts(n_conv + 2) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
+      // B fragments of one K step: rows of the current tap, chunk of channel step cs
+      int row[NBW], sw[NBW], nrow[NBW], nsw[NBW];
+      auto rows_for = [&](int tap, int(&rr)[NBW], int(&ss)[NBW]) {
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) tap_row<RB>(tap, in_off, OFF_Z, nb0 + n, l32, rr[n], ss[n]);
+      };
+      auto load_b = [&](const int(&rr)[NBW], const int(&ss)[NBW], int cs, frag_t(&dst)[NBW]) {
+        const int lc = MK == MK_F8 ? 4 * cs + 2 * lhi : 2 * cs + lhi;
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) dst[n] = lds_frag<MK>(smem, rr[n], ss[n], lc);
+      };
+      frag_t bc[NBW], bn[NBW];
+      rows_for(0, row, sw);
+      load_b(row, sw, 0, bc);
+
+      // One tap: CPT K steps in GPT prefetch groups; P0 = buffer of its first group.
+      // The first step of the layer starts its accumulators from zero.
+      auto tap_body = [&](auto p0_c, auto first_c, int tap) {
+        constexpr int P0 = decltype(p0_c)::value;
+        constexpr bool FIRST = decltype(first_c)::value;
+        // Branch-free body: after the last group of the network's last layer the
+        // prefetch re-reads this layer (never used); after the last tap the next
+        // tap's rows and fragments point inside the board or at the zero region.
+        const bool last_tap = tap == 8;
+        rows_for(tap + 1, nrow, nsw);
+        static_for<0, CPT>([&](auto cs_c) {
+          constexpr int cs = decltype(cs_c)::value;
+          constexpr int gs = cs / G, sg = cs % G;
+          constexpr int cur = P0 ^ (gs & 1);
+          auto& Acur = pick<cur>(A0, A1);
+          auto& Anext = pick<cur ^ 1>(A0, A1);
+          if constexpr (sg == 0) {
+            const uint8_t* nxt = wl + (size_t)(tap * CPT + (gs + 1) * G) * C::STEP_BYTES;
+            if constexpr (gs + 1 == GPT) nxt = (!last_tap || has_next) ? nxt : wl;
+            load_group(Anext, nxt);
+          }
+          if constexpr (cs + 1 < CPT) load_b(row, sw, cs + 1, bn);
+          else load_b(nrow, nsw, 0, bn);
+#pragma unroll
+          for (int m = 0; m < MBW; ++m)
+#pragma unroll
+            for (int n = 0; n < NBW; ++n)
+              c[m][n] = T::mma(Acur[sg][m], bc[n], (FIRST && cs == 0) ? acc_t{} : c[m][n]);
+#pragma unroll
+          for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
+          if constexpr (MK == MK_BF16) {
+            // interleave: one MFMA, then this step's LDS read and weight load
+            static_for<0, MBW * NBW>([&](auto i_c) {
+              constexpr int i = decltype(i_c)::value;
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              if constexpr (i < NBW) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+              if constexpr (sg == 0 && i < G * MBW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            });
+          }
+        });
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) {
+          row[n] = nrow[n];
+          sw[n] = nsw[n];
+        }
+      };
+      using IC0 = std::integral_constant<int, PAR>;
+      using IC1 = std::integral_constant<int, PAR ^ 1>;
+      tap_body(IC0{}, std::true_type{}, 0);
+      if constexpr (GPT % 2 == 1) {
+#pragma nounroll
+        for (int tap = 1; tap < 9; tap += 2) {
+          tap_body(IC1{}, std::false_type{}, tap);
+          tap_body(IC0{}, std::false_type{}, tap + 1);
+        }
+      } else {
+#pragma nounroll
+        for (int tap = 1; tap < 9; ++tap) tap_body(IC0{}, std::false_type{}, tap);
+      }
+
+      // epilogue
+      float hi = 0.0f, rq = 0.0f;
+      if constexpr (QUANT) {
+        hi = p.qhi[n_conv + 1];
+        rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
       }
 #pragma unroll
       for (int m = 0; m < MBW; ++m)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
-          const float4 bb = *reinterpret_cast<const float4*>(bias + ch0);
-          float4 mm = make_float4(1.f, 1.f, 1.f, 1.f);
-          if constexpr (MK != MK_BF16) mm = *reinterpret_cast<const float4*>(ms + ch0);
+          const float4 bb = *reinterpret_cast<const float4*>(kslot + ch0);
 #pragma unroll
           for (int n = 0; n < NBW; ++n) {
             const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
             const int rowo = out_off + (bl * 64 + j) * RB;
             const acc_t& v = c[m][n];
-            if constexpr (MK == MK_BF16) {
-              const int addr = rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi;
+            if constexpr (!QUANT) {
               float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
               float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
-              if (second) {
-                const uint2 r = *reinterpret_cast<const uint2*>(smem + addr);
-                y0 = y0 + bf16_lo(r.x);
-                y1 = y1 + bf16_hi(r.x);
-                y2 = y2 + bf16_lo(r.y);
-                y3 = y3 + bf16_hi(r.y);
+              if constexpr (SECOND) {
+                y0 = act_fn(y0 + res[m][n][4 * q + 0], cap);
+                y1 = act_fn(y1 + res[m][n][4 * q + 1], cap);
+                y2 = act_fn(y2 + res[m][n][4 * q + 2], cap);
+                y3 = act_fn(y3 + res[m][n][4 * q + 3], cap);
+                res[m][n][4 * q + 0] = y0;
+                res[m][n][4 * q + 1] = y1;
+                res[m][n][4 * q + 2] = y2;
+                res[m][n][4 * q + 3] = y3;
+              } else {
+                y0 = act_fn(y0, cap);
+                y1 = act_fn(y1, cap);
+                y2 = act_fn(y2, cap);
+                y3 = act_fn(y3, cap);
               }
-              *reinterpret_cast<uint2*>(smem + addr) =
-                  make_uint2(pack_bf16x2(act_fn(y0, cap), act_fn(y1, cap)),
-                             pack_bf16x2(act_fn(y2, cap), act_fn(y3, cap)));
+              *reinterpret_cast<uint2*>(smem + rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi) =
+                  make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
             } else {
+              const float4 mm = *reinterpret_cast<const float4*>(kslot + F + ch0);
               const int addr = rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15);
-              float y0 = (float)v[4 * q + 0] * mm.x, y1 = (float)v[4 * q + 1] * mm.y;
-              float y2 = (float)v[4 * q + 2] * mm.z, y3 = (float)v[4 * q + 3] * mm.w;
-              y0 = y0 + bb.x;
-              y1 = y1 + bb.y;
-              y2 = y2 + bb.z;
-              y3 = y3 + bb.w;
-              if (second) {
+              float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
+              float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
+              float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
+              float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
+              if constexpr (SECOND) {
                 const uint32_t r = *reinterpret_cast<const uint32_t*>(smem + addr);
-                y0 = y0 + dq_code<0>(MK, r) * a_res;
-                y1 = y1 + dq_code<1>(MK, r) * a_res;
-                y2 = y2 + dq_code<2>(MK, r) * a_res;
-                y3 = y3 + dq_code<3>(MK, r) * a_res;
+                z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
+                z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
+                z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
+                z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
               }
               *reinterpret_cast<uint32_t*>(smem + addr) =
-                  pack_q4(MK, act_fn(y0, cap) * inv_out, act_fn(y1, cap) * inv_out,
-                          act_fn(y2, cap) * inv_out, act_fn(y3, cap) * inv_out);
+                  pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi),
+                                 med3(z3, 0.0f, hi));
             }
           }
         }
+      if (has_next) store_consts((n_conv + 1) & 1, kn);
+      __syncthreads();
     };
 
-    auto body = [&](int g, frag_t(&cur)[G][MBW], frag_t(&nxt)[G][MBW]) {
-      if (g + 1 < NG) load(nxt, g + 1);
-      const int layer = g / GPL, gi = g - layer * GPL, tap = gi / GPT, gs = gi - tap * GPT;
-      const int in_off = (layer & 1) ? OFF_T : OFF_H;
-      if (gs == 0) tap_rows<RB, NBW>(tap, in_off, OFF_Z, nb0, l32, row, sw);
-#pragma unroll
-      for (int s = 0; s < G; ++s) {
-        const int cs = gs * G + s;
-        const int lc = MK == MK_F8 ? 4 * cs + 2 * lhi : 2 * cs + lhi;
-        frag_t bfr[NBW];
-#pragma unroll
-        for (int n = 0; n < NBW; ++n) bfr[n] = lds_frag<MK>(smem, row[n], sw[n], lc);
-#pragma unroll
-        for (int m = 0; m < MBW; ++m)
-#pragma unroll
-          for (int n = 0; n < NBW; ++n) c[m][n] = T::mma(cur[s][m], bfr[n], c[m][n]);
-      }
-      if (gi == GPL - 1) {
-        epilogue(layer);
-        __syncthreads();
-#pragma unroll
-        for (int m = 0; m < MBW; ++m)
-#pragma unroll
-          for (int n = 0; n < NBW; ++n) c[m][n] = acc_t{};
-      }
-    };
-
-    load(A0, 0);
-    for (int g = 0; g < NG; g += 2) {
-      body(g, A0, A1);
-      body(g + 1, A1, A0);
+    constexpr int PAR2 = GPL & 1;
+    for (int blk = 0; blk < p.blocks; ++blk) {
+      conv(std::false_type{}, std::integral_constant<int, 0>{}, 2 * blk);
+      conv(std::true_type{}, std::integral_constant<int, PAR2>{}, 2 * blk + 1);
     }
   }
 
@@ -417,27 +548,43 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
   const int LB = (P + 1) * 64;
   {
     constexpr int HS = F / 16, RBX = C::RBX, OFF_X = C::OFF_X, NBH = C::NBH;
+    if constexpr (QUANT) {
+      // codes -> exact bf16 values (int8 and e4m3 values are bf16-representable)
+      for (int idx = tid; idx < BPW * 64 * (F / 8); idx += NT) {
+        const int k = idx % (F / 8), sq = (idx / (F / 8)) & 63, bl = idx / (64 * (F / 8));
+        const uint2 v = *reinterpret_cast<const uint2*>(
+            smem + OFF_H + (bl * 64 + sq) * RB + (((k >> 1) ^ swz<RB>(sq)) << 4) + (k & 1) * 8);
+        const uint4 o = make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
+                                   pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
+                                   pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
+                                   pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y)));
+        *reinterpret_cast<uint4*>(smem + OFF_X + (bl * 64 + sq) * RBX + ((k ^ swz<RBX>(sq)) << 4)) = o;
+      }
+    } else {
+      // low half of the fp32 residual: bf16(h - bf16(h)), same layout at OFF_X
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
+#pragma unroll
+          for (int n = 0; n < NBW; ++n) {
+            const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
+            float lo[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) lo[r] = res[m][n][4 * q + r] - bf16_round(res[m][n][4 * q + r]);
+            *reinterpret_cast<uint2*>(smem + OFF_X + (bl * 64 + j) * RBX + (((ch0 >> 3) ^ swz<RBX>(j)) << 4) +
+                                      8 * lhi) = make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+          }
+        }
+    }
     SB::frag ha[HS][3];
     const uint8_t* hw = static_cast<const uint8_t*>(p.head_w) + (size_t)lane * 16;
 #pragma unroll
     for (int s = 0; s < HS; ++s)
 #pragma unroll
       for (int m = 0; m < 3; ++m) ha[s][m] = g_frag<MK_BF16>(hw + ((s * 3 + m) * 64) * 16);
-
-    if constexpr (MK != MK_BF16) {
-      // codes -> exact bf16 values (int8 and e4m3 values are bf16-representable)
-      for (int idx = tid; idx < BPW * 64 * (F / 8); idx += NT) {
-        const int k = idx % (F / 8), sq = (idx / (F / 8)) & 63, bl = idx / (64 * (F / 8));
-        const uint2 v = *reinterpret_cast<const uint2*>(
-            smem + OFF_H + (bl * 64 + sq) * RB + (((k >> 1) ^ swz<RB>(sq)) << 4) + (k & 1) * 8);
-        const uint4 o = make_uint4(pack_bf16x2(dq_code<0>(MK, v.x), dq_code<1>(MK, v.x)),
-                                   pack_bf16x2(dq_code<2>(MK, v.x), dq_code<3>(MK, v.x)),
-                                   pack_bf16x2(dq_code<0>(MK, v.y), dq_code<1>(MK, v.y)),
-                                   pack_bf16x2(dq_code<2>(MK, v.y), dq_code<3>(MK, v.y)));
-        *reinterpret_cast<uint4*>(smem + OFF_X + (bl * 64 + sq) * RBX + ((k ^ swz<RBX>(sq)) << 4)) = o;
-      }
-      __syncthreads();
-    }
+    __syncthreads();
 
     f32x16 hacc[NBH][3];
 #pragma unroll
@@ -454,11 +601,21 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
 #pragma unroll
           for (int m = 0; m < 3; ++m) hacc[k][m] = SB::mma(ha[s][m], bfr, hacc[k][m]);
         }
+        if constexpr (!QUANT) {
+          const int rowh = OFF_H + (bl * 64 + j) * RBX;
+#pragma unroll
+          for (int s = 0; s < HS; ++s) {
+            const SB::frag bfr = lds_frag<MK_BF16>(smem, rowh, swx, 2 * s + lhi);
+#pragma unroll
+            for (int m = 0; m < 3; ++m) hacc[k][m] = SB::mma(ha[s][m], bfr, hacc[k][m]);
+          }
+        }
       }
     }
     __syncthreads();
     float* L = reinterpret_cast<float*>(smem);
     const float hs = p.head_scale;
+    constexpr float LOG2E = 1.4426950408889634f;
 #pragma unroll
     for (int k = 0; k < NBH; ++k) {
       const int nb = w + k * NW;
@@ -469,7 +626,8 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int i = m * 32 + 8 * (v >> 2) + 4 * lhi + (v & 3);
-            if (i <= P) L[bl * LB + i * 64 + j] = hacc[k][m][v] * hs + p.head_b[i];
+            if (i < P) L[bl * LB + i * 64 + j] = (hacc[k][m][v] * hs + p.head_b[i]) * LOG2E;
+            else if (i == P) L[bl * LB + i * 64 + j] = hacc[k][m][v] * hs + p.head_b[i];
           }
       }
     }
@@ -487,50 +645,52 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
       const float* Lb = L + bl * LB;
       const uint8_t* lg = legal + (size_t)b * NM;
       float* pol = policy + (size_t)b * NM;
-      uint4 mk[NCH];
+      // logits are stored as z * log2(e): p_i = 2^(zl_i - max zl) / sum over legal cells.
+      // Illegal cells carry -inf through the max and contribute exactly 0.
+      float e[NCH][16];
       float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
         const int ch = lane + 64 * i;
-        mk[i] = make_uint4(0, 0, 0, 0);
         if (ch < n16) {
-          mk[i] = *reinterpret_cast<const uint4*>(lg + ch * 16);
-          const uint32_t wd[4] = {mk[i].x, mk[i].y, mk[i].z, mk[i].w};
+          const uint4 mk = *reinterpret_cast<const uint4*>(lg + ch * 16);
+          const uint32_t wd[4] = {mk.x, mk.y, mk.z, mk.w};
 #pragma unroll
-          for (int t = 0; t < 16; ++t)
-            if ((wd[t >> 2] >> (8 * (t & 3))) & 0xffu) mx = fmaxf(mx, Lb[ch * 16 + t]);
+          for (int t = 0; t < 16; t += 4) {
+            const float4 z4 = *reinterpret_cast<const float4*>(Lb + ch * 16 + t);
+            const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const bool ok = (wd[(t + u) >> 2] >> (8 * ((t + u) & 3))) & 0xffu;
+              e[i][t + u] = ok ? zz[u] : -INFINITY;
+              mx = fmaxf(mx, e[i][t + u]);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int t = 0; t < 16; ++t) e[i][t] = -INFINITY;
         }
       }
       mx = wave_max(mx);
+      const float msub = mx == -INFINITY ? 0.0f : mx;
       float sum = 0.0f;
-      if (mx != -INFINITY) {
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-          const int ch = lane + 64 * i;
-          if (ch < n16) {
-            const uint32_t wd[4] = {mk[i].x, mk[i].y, mk[i].z, mk[i].w};
+      for (int i = 0; i < NCH; ++i)
 #pragma unroll
-            for (int t = 0; t < 16; ++t)
-              if ((wd[t >> 2] >> (8 * (t & 3))) & 0xffu) sum += expf(Lb[ch * 16 + t] - mx);
-          }
+        for (int t = 0; t < 16; ++t) {
+          e[i][t] = __builtin_amdgcn_exp2f(e[i][t] - msub);  // exp2(-inf) = 0
+          sum += e[i][t];
         }
-      }
       sum = wave_sum(sum);
       const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
         const int ch = lane + 64 * i;
         if (ch < n16) {
-          const uint32_t wd[4] = {mk[i].x, mk[i].y, mk[i].z, mk[i].w};
-          float o[16];
-#pragma unroll
-          for (int t = 0; t < 16; ++t)
-            o[t] = ((wd[t >> 2] >> (8 * (t & 3))) & 0xffu) ? expf(Lb[ch * 16 + t] - mx) * inv : 0.0f;
           float4* dst = reinterpret_cast<float4*>(pol + ch * 16);
-          dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-          dst[1] = make_float4(o[4], o[5], o[6], o[7]);
-          dst[2] = make_float4(o[8], o[9], o[10], o[11]);
-          dst[3] = make_float4(o[12], o[13], o[14], o[15]);
+#pragma unroll
+          for (int t = 0; t < 16; t += 4)
+            dst[t / 4] = make_float4(e[i][t] * inv, e[i][t + 1] * inv, e[i][t + 2] * inv, e[i][t + 3] * inv);
         }
       }
       // value: u (64 squares) -> FC H -> ReLU -> FC 1 -> tanh
@@ -538,7 +698,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
 #pragma unroll
       for (int s = 0; s < 64; s += 4) {
         const float4 t4 = *reinterpret_cast<const float4*>(Lb + NM + s);
-        u[s] = t4.x; u[s + 1] = t4.y; u[s + 2] = t4.z; u[s + 3] = t4.w;
+        u[s] = t4.x;
+        u[s + 1] = t4.y;
+        u[s + 2] = t4.z;
+        u[s + 3] = t4.w;
       }
       if (p.value_conv_relu) {
 #pragma unroll
@@ -561,33 +724,38 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void az_net_kernel(
   }
 }
 
-template <int MK, int F, int MBW, int NBW, int WM, int WN, int G>
+template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC>
 hipError_t launch_cfg(const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
                       float* policy, float* value, hipStream_t s) {
-  using C = Cfg<MK, F, MBW, NBW, WM, WN, G>;
+  using C = Cfg<MK, F, MBW, NBW, WM, WN, G, OCC>;
   const int grid = (B + C::BPW - 1) / C::BPW;
-  hipLaunchKernelGGL((az_net_kernel<MK, F, MBW, NBW, WM, WN, G>), dim3(grid), dim3(C::NT), 0, s, n,
-                     planes, legal, B, policy, value);
+  hipLaunchKernelGGL((az_net_kernel<MK, F, MBW, NBW, WM, WN, G, OCC>), dim3(grid), dim3(C::NT), 0, s,
+                     n, planes, legal, B, policy, value);
   return hipGetLastError();
 }
 
-// Tilings.  Large: four boards per workgroup (two for F = 256), each wave a
-// 64-channel x 2-board tile.  Small: one board per workgroup.
+// Tilings (wave tile = MBW*32 channels x NBW half-boards):
+//   1 large:  4 boards per workgroup (2 for F = 256), 64 ch x 2 boards per wave
+//   2 small:  1 board per workgroup
+//   3 medium: 2 boards per workgroup, two workgroups per compute unit (F = 64, 128)
 template <int MK, int F>
 hipError_t launch_f(int tiling, const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
                     float* policy, float* value, hipStream_t s) {
   constexpr int CPT = F / Mk<MK>::KS;
-  constexpr int G = CPT < 8 ? CPT : 8;
+  // weight prefetch group: 4 K steps (2 for bf16, whose fp32 residual needs the registers)
+  constexpr int G = MK == MK_BF16 ? 2 : (CPT < 4 ? CPT : 4);
   if constexpr (F == 128) {
-    if (tiling == 1) return launch_cfg<MK, 128, 2, 4, 2, 2, G>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 128, 1, 2, 4, 1, G>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1) return launch_cfg<MK, 128, 2, 4, 2, 2, G, 1>(n, planes, legal, B, policy, value, s);
+    if (tiling == 3) return launch_cfg<MK, 128, 2, 2, 2, 2, G, 2>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 128, 1, 2, 4, 1, G, 2>(n, planes, legal, B, policy, value, s);
   } else if constexpr (F == 256) {
-    if (tiling == 1) return launch_cfg<MK, 256, 2, 4, 4, 1, G>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 256, 2, 2, 4, 1, G>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1) return launch_cfg<MK, 256, 2, 4, 4, 1, G, 1>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 256, 2, 2, 4, 1, G, 1>(n, planes, legal, B, policy, value, s);
   } else {
     static_assert(F == 64, "filters");
-    if (tiling == 1) return launch_cfg<MK, 64, 1, 4, 2, 2, G>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 64, 1, 2, 2, 1, G>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1) return launch_cfg<MK, 64, 1, 4, 2, 2, G, 1>(n, planes, legal, B, policy, value, s);
+    if (tiling == 3) return launch_cfg<MK, 64, 1, 2, 2, 2, G, 2>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 64, 1, 2, 2, 1, G, 2>(n, planes, legal, B, policy, value, s);
   }
 }
 
@@ -610,7 +778,12 @@ bool az_mfma_supported(int dtype, int filters) {
 
 int az_mfma_boards_per_wg(int filters, int tiling) {
   if (tiling == 2) return 1;
+  if (tiling == 3) return filters == 256 ? 1 : 2;
   return filters == 256 ? 2 : 4;
+}
+
+bool az_mfma_tiling_valid(int filters, int tiling) {
+  return tiling == 1 || tiling == 2 || (tiling == 3 && filters != 256);
 }
 
 hipError_t az_launch_mfma(int dtype, int tiling, const AzDevNet& n, const float* planes,

@@ -196,11 +196,17 @@ void pack_head(const BlobView& v, int F, int P, std::vector<uint8_t>& out) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Measured on MI355X (20x128 and 24x256 networks): one board per workgroup wins
+// below a few hundred boards; at 1024 boards the two-board medium tiling (two
+// workgroups per compute unit) wins for int8 / fp8 and the four-board large
+// tiling for bf16.
 int choose_tiling(const az_net* n, int B) {
   if (n->dtype == AZ_F32) return 0;
   if (n->tiling) return n->tiling;
-  const int bpw = az_mfma_boards_per_wg(n->spec.filters, 1);
-  return (B + bpw - 1) / bpw >= 256 ? 1 : 2;
+  const int F = n->spec.filters;
+  if (B < 512) return 2;
+  if (n->dtype == AZ_BF16) return B >= 1024 ? 1 : 2;
+  return az_mfma_tiling_valid(F, 3) ? 3 : 1;
 }
 
 }  // namespace
@@ -252,7 +258,7 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
 
   const BlobView v = view(spec, weights);
   std::vector<uint8_t> stem, tower, head;
-  std::vector<float> bias((size_t)(1 + 2 * NB) * F), mscale, act, inv;
+  std::vector<float> bias((size_t)(1 + 2 * NB) * F), qmul, qres, qhi;
   std::vector<float> head_b(AZ_HEAD_ROWS, 0.0f), fc2w(v.fc2_w, v.fc2_w + H);
   memcpy(bias.data(), v.stem_b, F * sizeof(float));
   for (int n = 0; n < 2 * NB; ++n) memcpy(bias.data() + (size_t)(1 + n) * F, v.b[n], F * sizeof(float));
@@ -274,12 +280,30 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
       for (int n = 0; n < 2 * NB; ++n) pack_conv(v.w[n], quant ? w_scales + (size_t)n * F : nullptr, F, F, F, kind, tower);
       pack_head(v, F, P, head);
       if (quant) {
-        mscale.resize((size_t)2 * NB * F);
+        // Requantising multiply-add constants; every product of two float32
+        // values is rounded once to float32, in this order.
+        const int K = 2 * NB + 1;
+        const float qmax = dtype == AZ_INT8 ? 127.0f : 448.0f;
+        std::vector<float> inv(K);
+        for (int k = 0; k < K; ++k) inv[k] = (float)(1.0 / (double)act_scales[k]);
+        qmul.resize((size_t)K * F);
+        qres.assign(K, 0.0f);
+        qhi.resize(K);
+        for (int f = 0; f < F; ++f) {
+          qmul[f] = inv[0];
+          bias[f] = v.stem_b[f] * inv[0];
+        }
         for (int n = 0; n < 2 * NB; ++n)
-          for (int f = 0; f < F; ++f) mscale[(size_t)n * F + f] = act_scales[n] * w_scales[(size_t)n * F + f];
-        act.assign(act_scales, act_scales + 2 * NB + 1);
-        inv.resize(2 * NB + 1);
-        for (int k = 0; k < 2 * NB + 1; ++k) inv[k] = (float)(1.0 / (double)act_scales[k]);
+          for (int f = 0; f < F; ++f) {
+            const float m = act_scales[n] * w_scales[(size_t)n * F + f];
+            qmul[(size_t)(1 + n) * F + f] = m * inv[n + 1];
+            bias[(size_t)(1 + n) * F + f] = v.b[n][f] * inv[n + 1];
+          }
+        for (int k = 0; k < K; ++k) {
+          if (k >= 2 && k % 2 == 0) qres[k] = act_scales[k - 2] * inv[k];
+          const float c = s.act_cap > 0.0f ? s.act_cap * inv[k] : qmax;
+          qhi[k] = c < qmax ? c : qmax;
+        }
       }
     }
   } catch (const std::bad_alloc&) {
@@ -290,8 +314,8 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   struct Sec { const void* src; size_t bytes; size_t off; };
   std::vector<Sec> secs = {
       {stem.data(), stem.size(), 0}, {tower.data(), tower.size(), 0}, {head.data(), head.size(), 0},
-      {bias.data(), bias.size() * 4, 0}, {mscale.data(), mscale.size() * 4, 0},
-      {act.data(), act.size() * 4, 0}, {inv.data(), inv.size() * 4, 0},
+      {bias.data(), bias.size() * 4, 0}, {qmul.data(), qmul.size() * 4, 0},
+      {qres.data(), qres.size() * 4, 0}, {qhi.data(), qhi.size() * 4, 0},
       {head_b.data(), head_b.size() * 4, 0}, {v.fc1_w, (size_t)H * 64 * 4, 0},
       {v.fc1_b, (size_t)H * 4, 0}, {fc2w.data(), fc2w.size() * 4, 0}};
   size_t total = 0;
@@ -330,9 +354,9 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   d.tower_w = at(1);
   d.head_w = at(2);
   d.bias = reinterpret_cast<const float*>(at(3));
-  d.mscale = reinterpret_cast<const float*>(at(4));
-  d.act = reinterpret_cast<const float*>(at(5));
-  d.inv = reinterpret_cast<const float*>(at(6));
+  d.qmul = reinterpret_cast<const float*>(at(4));
+  d.qres = reinterpret_cast<const float*>(at(5));
+  d.qhi = reinterpret_cast<const float*>(at(6));
   d.head_b = reinterpret_cast<const float*>(at(7));
   d.fc1_w = reinterpret_cast<const float*>(at(8));
   d.fc1_b = reinterpret_cast<const float*>(at(9));
@@ -368,7 +392,7 @@ int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_
 
 int az_net_set_tiling(az_net* net, int32_t tiling) {
   if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
-  if (net->dtype == AZ_F32 ? tiling != 0 : (tiling < 0 || tiling > 2))
+  if (net->dtype == AZ_F32 ? tiling != 0 : (tiling != 0 && !az_mfma_tiling_valid(net->spec.filters, tiling)))
     return fail(AZ_ERR_INVALID_ARG, "tiling %d not available for this dtype", tiling);
   net->tiling = tiling;
   return AZ_OK;
