@@ -7,7 +7,7 @@ heads + legal-move softmax + tanh value kernel.  Default workload: the 20-block,
 128-filter network (5,944,523 parameters) with int8 residual convolutions,
 batch 1024.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--tiling 0|1|2]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--tiling 0|1|2|3]
 
 Prints one JSON line on stdout.  --gpus N with N > 1 exits with a message: this
 library evaluates on one GPU (positions are independent; a multi-GPU server
@@ -17,6 +17,7 @@ would run one handle per GPU on its share of the batch).
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -31,6 +32,17 @@ import numpy as np  # noqa: E402
 import azgen  # noqa: E402
 
 CALIB = os.path.join(ROOT, "tests", "golden", "calib_net20x128_seed1004.npz")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_37447_amd", "csrc", "az_kernels_mfma.hip")
+
+# HBM traffic of the fused kernel from rocprofv3 --pmc passes (FETCH_SIZE, then
+# WRITE_SIZE, KiB per dispatch), scaled by what the same counters read for a plain
+# copy kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  An entry holds
+# for the kernel source it was taken on only: any other source reports null.
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
+TRAFFIC = {  # (workload, tiling): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
+    ("net20x128_int8_b1024", 3): ("2a8deb25cf03b496a3a2d1ea95606759ffd2105efa95b55ffde0db91f9ac14c4",
+                                  29536.6, 18704.0),
+}
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
 PEAK = {"bf16": 2.5e15, "int8": 5.0e15, "fp8": 5.0e15, "f32_vec": 157.3e12}
@@ -59,6 +71,17 @@ def roofline_peak(shape, dtype):
     flop = {k: 2.0 * v for k, v in m.items()}
     t_floor = sum(flop[k] / PEAK[unit[k]] for k in flop)
     return sum(flop.values()), sum(flop.values()) / t_floor
+
+
+def traffic_bytes(workload, tiling):
+    """Scaled HBM bytes per launch, or None without counters for this exact kernel."""
+    e = TRAFFIC.get((workload, tiling))
+    if e is None:
+        return None
+    with open(KERNEL_SRC, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != e[0]:
+            return None
+    return (e[1] * FETCH_SCALE + e[2] * WRITE_SCALE) * 1024.0
 
 
 def load_scales(w):
@@ -176,7 +199,7 @@ def main():
                    "params": w.shape.weight_count(), "flop_per_position": flop_pos},
         "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None},
+                     "traffic": traffic_bytes(w.name, tiling), "traffic_unit": "bytes per launch"},
         "outputs_valid": ok,
         "wall_s_timed": wall,
     }

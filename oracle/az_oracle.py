@@ -44,8 +44,10 @@ Modes.
                                and precision": most trunk convolutions in INT8,
                                the start block and heads at higher precision,
                                explicit quantise/dequantise operations).
-                               Products and sums are exact (float64 holds every
-                               integer and e4m3 product sum here); the steps that
+                               int8 products and sums are exact (float64 holds
+                               every such sum here); e4m3 dot products follow the
+                               matrix instruction's grouped precision (see
+                               conv3x3_fp8_hw); the steps that
                                decide a quantised code (rescale, bias, residual,
                                activation, requantise) are taken in float32 in a
                                fixed order, the same order the GPU kernels use.

@@ -445,7 +445,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
               c[m][n] = T::mma(Acur[sg][m], bc[n], (FIRST && cs == 0) ? acc_t{} : c[m][n]);
 #pragma unroll
           for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
-          if constexpr (MK == MK_BF16) {
+          if constexpr (MK == MK_BF16 && G == 2) {
             // interleave: one MFMA, then this step's LDS read and weight load
             static_for<0, MBW * NBW>([&](auto i_c) {
               constexpr int i = decltype(i_c)::value;
@@ -742,20 +742,23 @@ template <int MK, int F>
 hipError_t launch_f(int tiling, const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
                     float* policy, float* value, hipStream_t s) {
   constexpr int CPT = F / Mk<MK>::KS;
-  // weight prefetch group: 4 K steps (2 for bf16, whose fp32 residual needs the registers)
-  constexpr int G = MK == MK_BF16 ? 2 : (CPT < 4 ? CPT : 4);
+  // weight prefetch group: 4 K steps; 2 where the bf16 fp32 residual stream
+  // needs the registers (multi-board tilings, and every F = 256 tiling)
+  constexpr int G = CPT < 4 ? CPT : 4;
+  constexpr int GL = MK == MK_BF16 ? 2 : G;
+  constexpr int GS = MK == MK_BF16 && F == 256 ? 2 : G;
   if constexpr (F == 128) {
-    if (tiling == 1) return launch_cfg<MK, 128, 2, 4, 2, 2, G, 1>(n, planes, legal, B, policy, value, s);
-    if (tiling == 3) return launch_cfg<MK, 128, 2, 2, 2, 2, G, 2>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 128, 1, 2, 4, 1, G, 2>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1) return launch_cfg<MK, 128, 2, 4, 2, 2, GL, 1>(n, planes, legal, B, policy, value, s);
+    if (tiling == 3) return launch_cfg<MK, 128, 2, 2, 2, 2, GL, 2>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 128, 1, 2, 4, 1, GS, 2>(n, planes, legal, B, policy, value, s);
   } else if constexpr (F == 256) {
-    if (tiling == 1) return launch_cfg<MK, 256, 2, 4, 4, 1, G, 1>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 256, 2, 2, 4, 1, G, 1>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1) return launch_cfg<MK, 256, 2, 4, 4, 1, GL, 1>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 256, 2, 2, 4, 1, GS, 1>(n, planes, legal, B, policy, value, s);
   } else {
     static_assert(F == 64, "filters");
-    if (tiling == 1) return launch_cfg<MK, 64, 1, 4, 2, 2, G, 1>(n, planes, legal, B, policy, value, s);
-    if (tiling == 3) return launch_cfg<MK, 64, 1, 2, 2, 2, G, 2>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 64, 1, 2, 2, 1, G, 2>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1) return launch_cfg<MK, 64, 1, 4, 2, 2, GL, 1>(n, planes, legal, B, policy, value, s);
+    if (tiling == 3) return launch_cfg<MK, 64, 1, 2, 2, 2, GL, 2>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 64, 1, 2, 2, 1, GS, 2>(n, planes, legal, B, policy, value, s);
   }
 }
 
