@@ -40,6 +40,11 @@ struct AzDevNet {
   const float* fc1_b;   // [H]
   const float* fc2_w;   // [H]
   float fc2_b;
+  // MFMA kernels: per head row scale and bias (policy rows times log2(e), value
+  // row P as is, zero padding) and fc1 as [64/4][H][4] (see az_runtime.cpp)
+  const float* head_sc;  // [AZ_HEAD_ROWS]
+  const float* head_bc;  // [AZ_HEAD_ROWS]
+  const float* fc1_t;    // [16][H][4]
 };
 
 // Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small, 3 = medium.

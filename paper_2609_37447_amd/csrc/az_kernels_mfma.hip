@@ -86,6 +86,8 @@ template <> struct Mk<MK_F8> {
 };
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
+
 
 template <int I, int N, class F>
 __device__ __forceinline__ void static_for(F&& f) {
@@ -93,12 +95,6 @@ __device__ __forceinline__ void static_for(F&& f) {
     f(std::integral_constant<int, I>{});
     static_for<I + 1, N>(f);
   }
-}
-
-template <int I, class T>
-__device__ __forceinline__ T& pick(T& a, T& b) {
-  if constexpr (I == 0) return a;
-  else return b;
 }
 
 // Chunk swizzle for a row of RB bytes: rows of 256 bytes or more XOR with the
@@ -188,14 +184,16 @@ __device__ __forceinline__ void tap_row(int tap, int in_off, int zero_off, int n
   const int r = (j >> 3) + dy, c = (j & 7) + dx;
   const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
   const int src = r * 8 + c;
-  row = ok ? in_off + (bl * 64 + src) * RB_IN : zero_off + ((src * RB_IN) & 255);
+  const int ra = in_off + (bl * 64 + src) * RB_IN, rz = zero_off + ((src * RB_IN) & 255);
+  const int msk = -(int)ok;  // branch-free select keeps the tap loop one basic block
+  row = (ra & msk) | (rz & ~msk);
   sw = swz<RB_IN>(src);
 }
 
 // Tile shape: the wave owns MBW 32-channel blocks x NBW 32-square blocks; the
 // workgroup is WM x WN waves; G consecutive K steps form one weight prefetch
 // group; OCC workgroups share a compute unit.
-template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC>
+template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC, int NBUF_>
 struct Cfg {
   using T = Mk<MK>;
   static constexpr int NW = WM * WN, NT = 64 * NW;
@@ -213,24 +211,31 @@ struct Cfg {
   // per-layer epilogue constants, double-buffered: [2 slots][bias F | qmul F] floats
   static constexpr int OFF_K = 2 * BUF + ZB;
   static constexpr int KSLOT = 2 * F * 4;
-  static constexpr int SMEM =
-      cmax(cmax(OFF_K + 2 * KSLOT, OFF_X + BPW * 64 * RBX), BPW * LBMAX * 4);
+  // head row constants (scale, bias) and the softmax / value reductions sit past
+  // every other region: they are written at the start and read at the end
+  static constexpr int OFF_HC = (cmax(cmax(OFF_K + 2 * KSLOT, OFF_X + BPW * 64 * RBX), BPW * LBMAX * 4) + 15) & ~15;
+  static constexpr int RED_PER_BOARD = 32;  // floats: [0,8) sum groups, [8,12) max per wave, [16,24) value groups
+  static constexpr int OFF_RED = OFF_HC + 2 * AZ_HEAD_ROWS * 4;
+  static constexpr int SMEM = OFF_RED + BPW * RED_PER_BOARD * 4;
   static_assert(SMEM * OCC <= 160 * 1024, "LDS");
+  static_assert(NW % BPW == 0, "every board gets a whole number of waves at the end");
   static constexpr int CPT = F / T::KS;  // K steps per tap
   static_assert(CPT % G == 0, "group size");
   static constexpr int S = 9 * CPT;      // K steps per layer
   static constexpr int GPL = S / G;      // prefetch groups per layer
+  static constexpr int NBUF = NBUF_;     // weight prefetch ring depth (groups)
+  static_assert((2 * GPL) % NBUF == 0, "every block's first conv starts at ring slot 0");
   static constexpr int STEP_BYTES = NMB * 64 * T::FB;
   static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
   static constexpr int NBH = (2 * BPW + NW - 1) / NW;  // head N-blocks per wave
 };
 
-template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC>
+template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC, int NBUF_, int IL>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
                           amdgpu_waves_per_eu(OCC, OCC))) void
 az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal, int B,
               float* __restrict__ policy, float* __restrict__ value) {
-  using C = Cfg<MK, F, MBW, NBW, WM, WN, G, OCC>;
+  using C = Cfg<MK, F, MBW, NBW, WM, WN, G, OCC, NBUF_>;
   using T = typename C::T;
   using SB = Mk<MK_BF16>;
   using frag_t = typename T::frag;
@@ -271,15 +276,21 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   }
 
   // first weight group of the tower, in flight during the stem
+  // Weight fragments: a ring of NBUF prefetch groups; group g of a layer lives in
+  // buffer g % NBUF and is loaded NBUF - 1 groups before its use.
+  constexpr int NBUF = C::NBUF;
   const uint8_t* tw = static_cast<const uint8_t*>(p.tower_w) + (size_t)(mb0 * 64 + lane) * T::FB;
-  frag_t A0[G][MBW], A1[G][MBW];
+  frag_t A[NBUF][G][MBW];
   auto load_group = [&](frag_t(&dst)[G][MBW], const uint8_t* src) {
 #pragma unroll
     for (int s = 0; s < G; ++s)
 #pragma unroll
       for (int m = 0; m < MBW; ++m) dst[s][m] = g_frag<MK>(src + s * C::STEP_BYTES + m * 64 * T::FB);
   };
-  load_group(A0, tw);
+  static_for<0, NBUF - 1>([&](auto i_c) {
+    constexpr int i = decltype(i_c)::value;
+    load_group(A[i], tw + (size_t)i * G * C::STEP_BYTES);
+  });
   // per-layer epilogue constants: thread t < F/2 carries float4 t of [bias | qmul]
   auto load_consts = [&](int k) -> float4 {  // k = 1 + conv index (0 = stem)
     if (tid < F / 4) return *reinterpret_cast<const float4*>(p.bias + (size_t)k * F + tid * 4);
@@ -292,6 +303,10 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   };
   static_assert(NT >= F / 2, "constant staging needs F/2 threads");
   store_consts(0, load_consts(1));
+  if (tid < AZ_HEAD_ROWS / 2)  // [scale 96 | bias 96] floats
+    *reinterpret_cast<float4*>(smem + C::OFF_HC + tid * 16) =
+        *reinterpret_cast<const float4*>(tid < AZ_HEAD_ROWS / 4 ? p.head_sc + tid * 4 : p.head_bc + (tid - AZ_HEAD_ROWS / 4) * 4);
+  static_assert(NT >= AZ_HEAD_ROWS / 2, "head constant staging");
   __syncthreads();
 
   // ---- stem: bf16 3x3 conv over 32 (padded) input channels, K = 288
@@ -390,9 +405,9 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     acc_t c[MBW][NBW];
     const int nconv = 2 * p.blocks;
 
-    auto conv = [&](auto second_c, auto par_c, int n_conv) {
+    auto conv = [&](auto second_c, auto lb_c, int n_conv) {
       constexpr bool SECOND = decltype(second_c)::value;
-      constexpr int PAR = decltype(par_c)::value;
+      constexpr int LB = decltype(lb_c)::value;  // ring slot of the layer's first group
       const uint8_t* wl = tw + (size_t)n_conv * C::LAYER_BYTES;
       const bool has_next = n_conv + 1 < nconv;
       const int in_off = SECOND ? OFF_T : OFF_H;
@@ -415,26 +430,27 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       rows_for(0, row, sw);
       load_b(row, sw, 0, bc);
 
-      // One tap: CPT K steps in GPT prefetch groups; P0 = buffer of its first group.
-      // The first step of the layer starts its accumulators from zero.
-      auto tap_body = [&](auto p0_c, auto first_c, int tap) {
-        constexpr int P0 = decltype(p0_c)::value;
+      // One tap: CPT K steps in GPT prefetch groups; R0 = ring slot of its first
+      // group.  The first step of the layer starts its accumulators from zero.
+      auto tap_body = [&](auto r0_c, auto first_c, int tap) {
+        constexpr int R0 = decltype(r0_c)::value;
         constexpr bool FIRST = decltype(first_c)::value;
-        // Branch-free body: after the last group of the network's last layer the
-        // prefetch re-reads this layer (never used); after the last tap the next
-        // tap's rows and fragments point inside the board or at the zero region.
-        const bool last_tap = tap == 8;
+        // Branch-free body: prefetches past the network's last layer re-read this
+        // layer (never used); after the last tap the next tap's rows and fragments
+        // point inside the board or at the zero region.
         rows_for(tap + 1, nrow, nsw);
         static_for<0, CPT>([&](auto cs_c) {
           constexpr int cs = decltype(cs_c)::value;
           constexpr int gs = cs / G, sg = cs % G;
-          constexpr int cur = P0 ^ (gs & 1);
-          auto& Acur = pick<cur>(A0, A1);
-          auto& Anext = pick<cur ^ 1>(A0, A1);
+          constexpr int cur = (R0 + gs) % NBUF;
+          auto& Acur = A[cur];
           if constexpr (sg == 0) {
-            const uint8_t* nxt = wl + (size_t)(tap * CPT + (gs + 1) * G) * C::STEP_BYTES;
-            if constexpr (gs + 1 == GPT) nxt = (!last_tap || has_next) ? nxt : wl;
-            load_group(Anext, nxt);
+            // group tap*GPT + gs + NBUF-1 of this layer, i.e. of the next layer past
+            // the end (layers are contiguous)
+            const int gi = tap * GPT + gs + NBUF - 1;
+            const uint8_t* nxt = wl + (size_t)gi * G * C::STEP_BYTES;
+            nxt = (has_next || gi < GPL) ? nxt : wl;
+            load_group(A[(cur + NBUF - 1) % NBUF], nxt);
           }
           if constexpr (cs + 1 < CPT) load_b(row, sw, cs + 1, bn);
           else load_b(nrow, nsw, 0, bn);
@@ -445,13 +461,16 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
               c[m][n] = T::mma(Acur[sg][m], bc[n], (FIRST && cs == 0) ? acc_t{} : c[m][n]);
 #pragma unroll
           for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
-          if constexpr (MK == MK_BF16 && G == 2) {
-            // interleave: one MFMA, then this step's LDS read and weight load
-            static_for<0, MBW * NBW>([&](auto i_c) {
+          if constexpr (IL) {
+            // interleave: each MFMA is followed by one of the next step's LDS
+            // reads, then by one of the prefetch group's weight loads
+            constexpr int PER = MK == MK_F8 ? 2 : 1;  // instructions per fragment
+            constexpr int NDS = NBW * PER, NVM = sg == 0 ? G * MBW * PER : 0, NMF = MBW * NBW;
+            static_for<0, NMF>([&](auto i_c) {
               constexpr int i = decltype(i_c)::value;
               __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-              if constexpr (i < NBW) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-              if constexpr (sg == 0 && i < G * MBW) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+              if constexpr (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, i + 1 == NMF ? NDS - i : 1, 0);
+              if constexpr (i < NVM) __builtin_amdgcn_sched_group_barrier(0x020, i + 1 == NMF ? NVM - i : 1, 0);
             });
           }
         });
@@ -461,19 +480,22 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           sw[n] = nsw[n];
         }
       };
-      using IC0 = std::integral_constant<int, PAR>;
-      using IC1 = std::integral_constant<int, PAR ^ 1>;
-      tap_body(IC0{}, std::true_type{}, 0);
-      if constexpr (GPT % 2 == 1) {
+      // taps 1..8 in a runtime loop unrolled by U taps, U the period of the ring
+      // slot of a tap's first group; the remainder is peeled
+      constexpr int U = NBUF / gcd_c(GPT, NBUF), NIT = 8 / U, REM = 8 % U;
+      tap_body(std::integral_constant<int, LB>{}, std::true_type{}, 0);
 #pragma nounroll
-        for (int tap = 1; tap < 9; tap += 2) {
-          tap_body(IC1{}, std::false_type{}, tap);
-          tap_body(IC0{}, std::false_type{}, tap + 1);
-        }
-      } else {
-#pragma nounroll
-        for (int tap = 1; tap < 9; ++tap) tap_body(IC0{}, std::false_type{}, tap);
+      for (int it = 0; it < NIT; ++it) {
+        static_for<0, U>([&](auto u_c) {
+          constexpr int u = decltype(u_c)::value;
+          tap_body(std::integral_constant<int, (LB + (1 + u) * GPT) % NBUF>{}, std::false_type{},
+                   1 + it * U + u);
+        });
       }
+      static_for<0, REM>([&](auto u_c) {
+        constexpr int u = decltype(u_c)::value, t = 1 + NIT * U + u;
+        tap_body(std::integral_constant<int, (LB + t * GPT) % NBUF>{}, std::false_type{}, t);
+      });
 
       // epilogue
       float hi = 0.0f, rq = 0.0f;
@@ -481,71 +503,112 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         hi = p.qhi[n_conv + 1];
         rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
       }
+      // The epilogue walks the wave's rows in runs k = (m, q) of 4 channels.  Its
+      // LDS reads (the run's per-channel constants and, for the second conv of
+      // a quantised block, the residual codes, read in place before this lane
+      // overwrites them) are issued EP_AHEAD runs ahead of their arithmetic, in
+      // a ring of EP_AHEAD + 1 slots, so that no read latency is exposed.
+      constexpr int NRUN = MBW * 4, EP_AHEAD = QUANT ? 2 : 0, EP_RING = EP_AHEAD + 1;
+      constexpr bool RCODE = QUANT && SECOND;
+      float4 kb[EP_RING], km[QUANT ? EP_RING : 1];
+      uint32_t rcode[RCODE ? EP_RING : 1][RCODE ? NBW : 1];
+      auto ep_addr = [&](int m, int q, int n) {
+        const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
+        const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
+        const int rowo = out_off + (bl * 64 + j) * RB;
+        if constexpr (QUANT) return rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15);
+        else return rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi;
+      };
+      auto ep_load = [&](auto k_c) {
+        constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
+        const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
+        kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
+        if constexpr (QUANT) km[slot] = *reinterpret_cast<const float4*>(kslot + F + ch0);
+        if constexpr (RCODE) {
 #pragma unroll
-      for (int m = 0; m < MBW; ++m)
+          for (int n = 0; n < NBW; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
+        }
+      };
+      static_for<0, EP_AHEAD>([&](auto k_c) { ep_load(k_c); });
+      static_for<0, NRUN>([&](auto k_c) {
+        constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
+        if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
+        const float4 bb = kb[slot];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
-          const float4 bb = *reinterpret_cast<const float4*>(kslot + ch0);
-#pragma unroll
-          for (int n = 0; n < NBW; ++n) {
-            const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
-            const int rowo = out_off + (bl * 64 + j) * RB;
-            const acc_t& v = c[m][n];
-            if constexpr (!QUANT) {
-              float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
-              float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
-              if constexpr (SECOND) {
-                y0 = act_fn(y0 + res[m][n][4 * q + 0], cap);
-                y1 = act_fn(y1 + res[m][n][4 * q + 1], cap);
-                y2 = act_fn(y2 + res[m][n][4 * q + 2], cap);
-                y3 = act_fn(y3 + res[m][n][4 * q + 3], cap);
-                res[m][n][4 * q + 0] = y0;
-                res[m][n][4 * q + 1] = y1;
-                res[m][n][4 * q + 2] = y2;
-                res[m][n][4 * q + 3] = y3;
-              } else {
-                y0 = act_fn(y0, cap);
-                y1 = act_fn(y1, cap);
-                y2 = act_fn(y2, cap);
-                y3 = act_fn(y3, cap);
-              }
-              *reinterpret_cast<uint2*>(smem + rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi) =
-                  make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+        for (int n = 0; n < NBW; ++n) {
+          const int addr = ep_addr(m, q, n);
+          const acc_t& v = c[m][n];
+          if constexpr (!QUANT) {
+            float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
+            float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
+            if constexpr (SECOND) {
+              y0 = act_fn(y0 + res[m][n][4 * q + 0], cap);
+              y1 = act_fn(y1 + res[m][n][4 * q + 1], cap);
+              y2 = act_fn(y2 + res[m][n][4 * q + 2], cap);
+              y3 = act_fn(y3 + res[m][n][4 * q + 3], cap);
+              res[m][n][4 * q + 0] = y0;
+              res[m][n][4 * q + 1] = y1;
+              res[m][n][4 * q + 2] = y2;
+              res[m][n][4 * q + 3] = y3;
             } else {
-              const float4 mm = *reinterpret_cast<const float4*>(kslot + F + ch0);
-              const int addr = rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15);
-              float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
-              float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
-              float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
-              float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
-              if constexpr (SECOND) {
-                const uint32_t r = *reinterpret_cast<const uint32_t*>(smem + addr);
-                z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
-                z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
-                z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
-                z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
-              }
-              *reinterpret_cast<uint32_t*>(smem + addr) =
-                  pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi),
-                                 med3(z3, 0.0f, hi));
+              y0 = act_fn(y0, cap);
+              y1 = act_fn(y1, cap);
+              y2 = act_fn(y2, cap);
+              y3 = act_fn(y3, cap);
             }
+            *reinterpret_cast<uint2*>(smem + addr) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+          } else {
+            const float4 mm = km[slot];
+            float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
+            float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
+            float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
+            float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
+            if constexpr (SECOND) {
+              const uint32_t r = rcode[slot][n];
+              z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
+              z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
+              z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
+              z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
+            }
+            *reinterpret_cast<uint32_t*>(smem + addr) =
+                pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi), med3(z3, 0.0f, hi));
           }
         }
+      });
       if (has_next) store_consts((n_conv + 1) & 1, kn);
       __syncthreads();
     };
 
-    constexpr int PAR2 = GPL & 1;
     for (int blk = 0; blk < p.blocks; ++blk) {
       conv(std::false_type{}, std::integral_constant<int, 0>{}, 2 * blk);
-      conv(std::true_type{}, std::integral_constant<int, PAR2>{}, 2 * blk + 1);
+      conv(std::true_type{}, std::integral_constant<int, GPL % NBUF>{}, 2 * blk + 1);
     }
   }
 
   // ---- heads: 1x1 convs F -> (P policy planes + 1 value row) as one bf16 GEMM
   const int P = p.policy_planes;
   const int LB = (P + 1) * 64;
+  const int NMV = P * 64;
+  // Softmax and value: WPB waves per board.  The board's cells form groups g of
+  // 1024; in group g lane l owns the four runs of 4 cells at g*1024 + u*256 + 4l
+  // (u = 0..3), so that a wave's LDS reads, mask loads and policy stores are
+  // contiguous.  Wave part p of the board takes groups p, p + WPB, ...  Its
+  // legal mask is loaded here, in flight during the heads.
+  constexpr int WPB = NW / BPW;
+  constexpr int NGRP = (AZ_MAX_POLICY * 64 + 1023) / 1024;  // cell groups
+  constexpr int NGW = (NGRP + WPB - 1) / WPB;               // groups per wave
+  const int sbl = w / WPB, spart = w % WPB;
+  const int sb = b0 + sbl;
+  const bool svalid = sb < B;
+  uint32_t mk0[NGW][4];
+#pragma unroll
+  for (int ii = 0; ii < NGW; ++ii)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = 1024 * (spart + WPB * ii) + 256 * u + 4 * lane;
+      mk0[ii][u] = 0u;
+      if (svalid && c < NMV) mk0[ii][u] = *reinterpret_cast<const uint32_t*>(legal + (size_t)sb * NMV + c);
+    }
   {
     constexpr int HS = F / 16, RBX = C::RBX, OFF_X = C::OFF_X, NBH = C::NBH;
     if constexpr (QUANT) {
@@ -613,126 +676,166 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       }
     }
     __syncthreads();
+    // every row of every board: fma(acc, scale, bias) with the row constants
+    // (policy rows leave pre-scaled by log2(e), rows past P are never read)
     float* L = reinterpret_cast<float*>(smem);
-    const float hs = p.head_scale;
-    constexpr float LOG2E = 1.4426950408889634f;
+    const float* HC = reinterpret_cast<const float*>(smem + C::OFF_HC);
 #pragma unroll
-    for (int k = 0; k < NBH; ++k) {
-      const int nb = w + k * NW;
-      if (nb < 2 * BPW) {
-        const int bl = nb >> 1, j = ((nb & 1) << 5) + l32;
+    for (int m = 0; m < 3; ++m)
 #pragma unroll
-        for (int m = 0; m < 3; ++m)
+      for (int q = 0; q < 4; ++q) {
+        const int r0 = m * 32 + 8 * q + 4 * lhi;
+        const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+        const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_HEAD_ROWS + r0);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int i = m * 32 + 8 * (v >> 2) + 4 * lhi + (v & 3);
-            if (i < P) L[bl * LB + i * 64 + j] = (hacc[k][m][v] * hs + p.head_b[i]) * LOG2E;
-            else if (i == P) L[bl * LB + i * 64 + j] = hacc[k][m][v] * hs + p.head_b[i];
+        for (int k = 0; k < NBH; ++k) {
+          const int nb = w + k * NW;
+          if (nb < 2 * BPW) {
+            const int bl = nb >> 1, j = ((nb & 1) << 5) + l32;
+            float* dst = L + bl * C::LBMAX + r0 * 64 + j;
+            dst[0] = __builtin_fmaf(hacc[k][m][4 * q + 0], sc.x, bc.x);
+            dst[64] = __builtin_fmaf(hacc[k][m][4 * q + 1], sc.y, bc.y);
+            dst[128] = __builtin_fmaf(hacc[k][m][4 * q + 2], sc.z, bc.z);
+            dst[192] = __builtin_fmaf(hacc[k][m][4 * q + 3], sc.w, bc.w);
           }
+        }
       }
-    }
   }
   __syncthreads();
 
-  // ---- legal-move softmax and value head: one wave per board
+  // ---- legal-move softmax and value head: WPB waves per board (board sbl, part spart)
+  // Sums are taken in an order that does not depend on WPB, so every tiling
+  // returns the same bits: each 64-chunk group (policy) or 64-unit group (value
+  // hidden layer) is reduced across the lanes of one wave, and the group sums
+  // are added in group order.
   {
     const float* L = reinterpret_cast<const float*>(smem);
-    const int NM = P * 64, n16 = NM >> 4, H = p.value_hidden;
-    constexpr int NCH = (AZ_MAX_POLICY * 4 + 63) / 64;
-    for (int bl = w; bl < BPW; bl += NW) {
-      const int b = b0 + bl;
-      if (b >= B) continue;
-      const float* Lb = L + bl * LB;
-      const uint8_t* lg = legal + (size_t)b * NM;
-      float* pol = policy + (size_t)b * NM;
-      // logits are stored as z * log2(e): p_i = 2^(zl_i - max zl) / sum over legal cells.
-      // Illegal cells carry -inf through the max and contribute exactly 0.
-      float e[NCH][16];
-      float mx = -INFINITY;
+    float* red = reinterpret_cast<float*>(smem + C::OFF_RED) + sbl * C::RED_PER_BOARD;
+    const float* Lb = L + sbl * C::LBMAX;
+    float* pol = policy + (size_t)sb * NMV;
+    const int H = p.value_hidden;
+    // logits are stored as z * log2(e): p_i = 2^(zl_i - max zl) / sum over legal cells.
+    // Illegal cells carry -inf through the max and contribute exactly 0.
+    float e[NGW][16];
+    float mx = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < NCH; ++i) {
-        const int ch = lane + 64 * i;
-        if (ch < n16) {
-          const uint4 mk = *reinterpret_cast<const uint4*>(lg + ch * 16);
-          const uint32_t wd[4] = {mk.x, mk.y, mk.z, mk.w};
+    for (int ii = 0; ii < NGW; ++ii)
 #pragma unroll
-          for (int t = 0; t < 16; t += 4) {
-            const float4 z4 = *reinterpret_cast<const float4*>(Lb + ch * 16 + t);
-            const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
+      for (int u = 0; u < 4; ++u) {
+        const int c = 1024 * (spart + WPB * ii) + 256 * u + 4 * lane;
+        const bool in = c < NMV;
+        const float4 z4 = in ? *reinterpret_cast<const float4*>(Lb + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const bool ok = (wd[(t + u) >> 2] >> (8 * ((t + u) & 3))) & 0xffu;
-              e[i][t + u] = ok ? zz[u] : -INFINITY;
-              mx = fmaxf(mx, e[i][t + u]);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int t = 0; t < 16; ++t) e[i][t] = -INFINITY;
+        for (int t = 0; t < 4; ++t) {
+          const bool ok = in && ((mk0[ii][u] >> (8 * t)) & 0xffu);
+          e[ii][4 * u + t] = ok ? zz[t] : -INFINITY;
+          mx = fmaxf(mx, e[ii][4 * u + t]);
         }
       }
-      mx = wave_max(mx);
-      const float msub = mx == -INFINITY ? 0.0f : mx;
-      float sum = 0.0f;
+    mx = wave_max(mx);
+    if (lane == 0) red[8 + spart] = mx;
+    __syncthreads();
+    float bmx = red[8];
 #pragma unroll
-      for (int i = 0; i < NCH; ++i)
+    for (int t = 1; t < WPB; ++t) bmx = fmaxf(bmx, red[8 + t]);
+    const float msub = bmx == -INFINITY ? 0.0f : bmx;
 #pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          e[i][t] = __builtin_amdgcn_exp2f(e[i][t] - msub);  // exp2(-inf) = 0
-          sum += e[i][t];
+    for (int ii = 0; ii < NGW; ++ii) {
+      float gsum = 0.0f;
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        e[ii][t] = __builtin_amdgcn_exp2f(e[ii][t] - msub);  // exp2(-inf) = 0
+        gsum += e[ii][t];
+      }
+      gsum = wave_sum(gsum);
+      if (lane == 0 && spart + WPB * ii < NGRP) red[spart + WPB * ii] = gsum;
+    }
+    // value head inputs and hidden-unit groups r (unit 64 r + lane) of this wave
+    float u[64];
+#pragma unroll
+    for (int s4 = 0; s4 < 64; s4 += 4) {
+      const float4 t4 = *reinterpret_cast<const float4*>(Lb + NMV + s4);
+      u[s4] = t4.x;
+      u[s4 + 1] = t4.y;
+      u[s4 + 2] = t4.z;
+      u[s4 + 3] = t4.w;
+    }
+    if (p.value_conv_relu) {
+#pragma unroll
+      for (int s4 = 0; s4 < 64; ++s4) u[s4] = fmaxf(u[s4], 0.0f);
+    }
+    const int ngv = (H + 63) >> 6;  // hidden-unit groups (H <= 512: at most 8)
+    for (int r = spart; r < ngv; r += WPB) {
+      const int k = 64 * r + lane;
+      const bool ok = k < H;
+      const float4* src = reinterpret_cast<const float4*>(p.fc1_t) + (ok ? k : 0);
+      float4 wr[16];
+#pragma unroll
+      for (int s4 = 0; s4 < 16; ++s4) wr[s4] = src[(size_t)s4 * H];
+      float g = ok ? p.fc1_b[k] : 0.0f;
+      const float w2 = ok ? p.fc2_w[k] : 0.0f;
+#pragma unroll
+      for (int s4 = 0; s4 < 16; ++s4)
+        g += wr[s4].x * u[4 * s4] + wr[s4].y * u[4 * s4 + 1] + wr[s4].z * u[4 * s4 + 2] + wr[s4].w * u[4 * s4 + 3];
+      const float vsum = wave_sum(w2 * fmaxf(g, 0.0f));
+      if (lane == 0) red[16 + r] = vsum;
+    }
+    __syncthreads();
+    float tot = 0.0f;
+#pragma unroll
+    for (int g = 0; g < NGRP; ++g) tot += (1024 * g < NMV) ? red[g] : 0.0f;
+    const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+    if (svalid) {
+#pragma unroll
+      for (int ii = 0; ii < NGW; ++ii)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int c = 1024 * (spart + WPB * ii) + 256 * u + 4 * lane;
+          if (c < NMV)
+            *reinterpret_cast<float4*>(pol + c) =
+                make_float4(e[ii][4 * u] * inv, e[ii][4 * u + 1] * inv, e[ii][4 * u + 2] * inv, e[ii][4 * u + 3] * inv);
         }
-      sum = wave_sum(sum);
-      const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
-#pragma unroll
-      for (int i = 0; i < NCH; ++i) {
-        const int ch = lane + 64 * i;
-        if (ch < n16) {
-          float4* dst = reinterpret_cast<float4*>(pol + ch * 16);
-#pragma unroll
-          for (int t = 0; t < 16; t += 4)
-            dst[t / 4] = make_float4(e[i][t] * inv, e[i][t + 1] * inv, e[i][t + 2] * inv, e[i][t + 3] * inv);
-        }
+      if (spart == 0 && lane == 0) {
+        float vs = 0.0f;
+        for (int r = 0; r < ngv; ++r) vs += red[16 + r];
+        value[sb] = tanhf(vs + p.fc2_b);
       }
-      // value: u (64 squares) -> FC H -> ReLU -> FC 1 -> tanh
-      float u[64];
-#pragma unroll
-      for (int s = 0; s < 64; s += 4) {
-        const float4 t4 = *reinterpret_cast<const float4*>(Lb + NM + s);
-        u[s] = t4.x;
-        u[s + 1] = t4.y;
-        u[s + 2] = t4.z;
-        u[s + 3] = t4.w;
-      }
-      if (p.value_conv_relu) {
-#pragma unroll
-        for (int s = 0; s < 64; ++s) u[s] = fmaxf(u[s], 0.0f);
-      }
-      float part = 0.0f;
-      for (int k = lane; k < H; k += 64) {
-        const float4* wr = reinterpret_cast<const float4*>(p.fc1_w + (size_t)k * 64);
-        float g = p.fc1_b[k];
-#pragma unroll
-        for (int s = 0; s < 16; ++s) {
-          const float4 ww = wr[s];
-          g += ww.x * u[4 * s] + ww.y * u[4 * s + 1] + ww.z * u[4 * s + 2] + ww.w * u[4 * s + 3];
-        }
-        part += p.fc2_w[k] * fmaxf(g, 0.0f);
-      }
-      part = wave_sum(part);
-      if (lane == 0) value[b] = tanhf(part + p.fc2_b);
     }
   }
 }
 
-template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC>
+template <int MK, int F, int MBW, int NBW, int WM, int WN, int G, int OCC, int NBUF, int IL>
 hipError_t launch_cfg(const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
                       float* policy, float* value, hipStream_t s) {
-  using C = Cfg<MK, F, MBW, NBW, WM, WN, G, OCC>;
+  using C = Cfg<MK, F, MBW, NBW, WM, WN, G, OCC, NBUF>;
   const int grid = (B + C::BPW - 1) / C::BPW;
-  hipLaunchKernelGGL((az_net_kernel<MK, F, MBW, NBW, WM, WN, G, OCC>), dim3(grid), dim3(C::NT), 0, s,
+  hipLaunchKernelGGL((az_net_kernel<MK, F, MBW, NBW, WM, WN, G, OCC, NBUF, IL>), dim3(grid), dim3(C::NT), 0, s,
                      n, planes, legal, B, policy, value);
   return hipGetLastError();
 }
+
+// K-loop weight stream per tiling: G-step prefetch groups, a ring of NB groups
+// (loaded NB-1 groups ahead), IL = explicit MFMA / LDS / load interleave.
+// Deepest ring of at most `want` groups that tiles two layers of `gpl` groups.
+constexpr int ring_depth(int want, int gpl) {
+  return want <= 2 ? 2 : ((2 * gpl) % want == 0 ? want : ring_depth(want - 1, gpl));
+}
+
+template <int MK, int F>
+struct Sched {
+  static constexpr int CPT = F / Mk<MK>::KS;
+  static constexpr bool BF = MK == MK_BF16;
+  // Multi-board tilings: int8 streams one step per group with a ring of 8
+  // (7 steps of prefetch), fp8 (32-byte fragments) a ring of 4, bf16 two-step
+  // groups with a ring of 2 (its fp32 residual stream needs the registers).
+  static constexpr int GL = BF ? 2 : 1, NL = BF ? 2 : (MK == MK_I8 ? 8 : 4), IL_L = 1;
+  static constexpr int GM = GL, NM = NL, IL_M = 1;
+  // small (one board per workgroup): one-step groups, ring of 8, except bf16 at
+  // F = 256, whose wider tile needs the registers for its residual stream
+  static constexpr bool W256 = BF && F == 256;
+  static constexpr int GS = W256 ? 2 : 1, NS = W256 ? 2 : 8, IL_S = 1;
+};
 
 // Tilings (wave tile = MBW*32 channels x NBW half-boards):
 //   1 large:  4 boards per workgroup (2 for F = 256), 64 ch x 2 boards per wave
@@ -741,24 +844,24 @@ hipError_t launch_cfg(const AzDevNet& n, const float* planes, const uint8_t* leg
 template <int MK, int F>
 hipError_t launch_f(int tiling, const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
                     float* policy, float* value, hipStream_t s) {
-  constexpr int CPT = F / Mk<MK>::KS;
-  // weight prefetch group: 4 K steps; 2 where the bf16 fp32 residual stream
-  // needs the registers (multi-board tilings, and every F = 256 tiling)
-  constexpr int G = CPT < 4 ? CPT : 4;
-  constexpr int GL = MK == MK_BF16 ? 2 : G;
-  constexpr int GS = MK == MK_BF16 && F == 256 ? 2 : G;
+  using S = Sched<MK, F>;
   if constexpr (F == 128) {
-    if (tiling == 1) return launch_cfg<MK, 128, 2, 4, 2, 2, GL, 1>(n, planes, legal, B, policy, value, s);
-    if (tiling == 3) return launch_cfg<MK, 128, 2, 2, 2, 2, GL, 2>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 128, 1, 2, 4, 1, GS, 2>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1)
+      return launch_cfg<MK, 128, 2, 4, 2, 2, S::GL, 1, ring_depth(S::NL, 9 * S::CPT / S::GL), S::IL_L>(n, planes, legal, B, policy, value, s);
+    if (tiling == 3)
+      return launch_cfg<MK, 128, 2, 2, 2, 2, S::GM, 2, ring_depth(S::NM, 9 * S::CPT / S::GM), S::IL_M>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 128, 1, 2, 4, 1, S::GS, 2, ring_depth(S::NS, 9 * S::CPT / S::GS), S::IL_S>(n, planes, legal, B, policy, value, s);
   } else if constexpr (F == 256) {
-    if (tiling == 1) return launch_cfg<MK, 256, 2, 4, 4, 1, GL, 1>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 256, 2, 2, 4, 1, GS, 1>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1)
+      return launch_cfg<MK, 256, 2, 4, 4, 1, S::GL, 1, ring_depth(S::NL, 9 * S::CPT / S::GL), S::IL_L>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 256, 2, 2, 4, 1, S::GS, 1, ring_depth(S::NS, 9 * S::CPT / S::GS), S::IL_S>(n, planes, legal, B, policy, value, s);
   } else {
     static_assert(F == 64, "filters");
-    if (tiling == 1) return launch_cfg<MK, 64, 1, 4, 2, 2, GL, 1>(n, planes, legal, B, policy, value, s);
-    if (tiling == 3) return launch_cfg<MK, 64, 1, 2, 2, 2, GL, 2>(n, planes, legal, B, policy, value, s);
-    return launch_cfg<MK, 64, 1, 2, 2, 1, GS, 2>(n, planes, legal, B, policy, value, s);
+    if (tiling == 1)
+      return launch_cfg<MK, 64, 1, 4, 2, 2, S::GL, 1, ring_depth(S::NL, 9 * S::CPT / S::GL), S::IL_L>(n, planes, legal, B, policy, value, s);
+    if (tiling == 3)
+      return launch_cfg<MK, 64, 1, 2, 2, 2, S::GM, 2, ring_depth(S::NM, 9 * S::CPT / S::GM), S::IL_M>(n, planes, legal, B, policy, value, s);
+    return launch_cfg<MK, 64, 1, 2, 2, 1, S::GS, 2, ring_depth(S::NS, 9 * S::CPT / S::GS), S::IL_S>(n, planes, legal, B, policy, value, s);
   }
 }
 

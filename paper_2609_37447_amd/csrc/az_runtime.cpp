@@ -258,13 +258,33 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
 
   const BlobView v = view(spec, weights);
   std::vector<uint8_t> stem, tower, head;
-  std::vector<float> bias((size_t)(1 + 2 * NB) * F), qmul, qres, qhi;
-  std::vector<float> head_b(AZ_HEAD_ROWS, 0.0f), fc2w(v.fc2_w, v.fc2_w + H);
-  memcpy(bias.data(), v.stem_b, F * sizeof(float));
-  for (int n = 0; n < 2 * NB; ++n) memcpy(bias.data() + (size_t)(1 + n) * F, v.b[n], F * sizeof(float));
-  for (int i = 0; i < P; ++i) head_b[i] = v.pol_b[i];
-  head_b[P] = v.val_b[0];
+  std::vector<float> bias, qmul, qres, qhi, head_b, fc2w, head_sc, head_bc, fc1t;
+  const float hs = quant ? act_scales[2 * NB] : 1.0f;
   try {
+    bias.resize((size_t)(1 + 2 * NB) * F);
+    head_b.assign(AZ_HEAD_ROWS, 0.0f);
+    fc2w.assign(v.fc2_w, v.fc2_w + H);
+    memcpy(bias.data(), v.stem_b, F * sizeof(float));
+    for (int n = 0; n < 2 * NB; ++n) memcpy(bias.data() + (size_t)(1 + n) * F, v.b[n], F * sizeof(float));
+    for (int i = 0; i < P; ++i) head_b[i] = v.pol_b[i];
+    head_b[P] = v.val_b[0];
+    // MFMA kernels: every head row r stores fma(acc, head_sc[r], head_bc[r]); policy
+    // rows come out pre-scaled by log2(e) for the exp2 softmax, the value row P
+    // unscaled, padding rows zero.  Products rounded once to float32.
+    const float log2e = 1.4426950408889634f;
+    head_sc.assign(AZ_HEAD_ROWS, 0.0f);
+    head_bc.assign(AZ_HEAD_ROWS, 0.0f);
+    for (int i = 0; i < P; ++i) {
+      head_sc[i] = hs * log2e;
+      head_bc[i] = v.pol_b[i] * log2e;
+    }
+    head_sc[P] = hs;
+    head_bc[P] = v.val_b[0];
+    // fc1 for the MFMA kernels as [64/4][H][4]: lane k of a wave reads
+    // W1[k][4s .. 4s+3] at ((s * H + k) * 4), so a wave's float4 loads are contiguous.
+    fc1t.resize((size_t)H * 64);
+    for (int k = 0; k < H; ++k)
+      for (int c = 0; c < 64; ++c) fc1t[((size_t)(c / 4) * H + k) * 4 + (c % 4)] = v.fc1_w[(size_t)k * 64 + c];
     if (dtype == AZ_F32) {
       stem.resize((size_t)F * Cin * 9 * 4);
       memcpy(stem.data(), v.stem_w, stem.size());
@@ -317,7 +337,9 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
       {bias.data(), bias.size() * 4, 0}, {qmul.data(), qmul.size() * 4, 0},
       {qres.data(), qres.size() * 4, 0}, {qhi.data(), qhi.size() * 4, 0},
       {head_b.data(), head_b.size() * 4, 0}, {v.fc1_w, (size_t)H * 64 * 4, 0},
-      {v.fc1_b, (size_t)H * 4, 0}, {fc2w.data(), fc2w.size() * 4, 0}};
+      {v.fc1_b, (size_t)H * 4, 0}, {fc2w.data(), fc2w.size() * 4, 0},
+      {head_sc.data(), head_sc.size() * 4, 0}, {head_bc.data(), head_bc.size() * 4, 0},
+      {fc1t.data(), fc1t.size() * 4, 0}};
   size_t total = 0;
   for (auto& sc : secs) { sc.off = total; total += align256(sc.bytes); }
 
@@ -349,7 +371,7 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   d.value_hidden = H;
   d.value_conv_relu = s.value_conv_relu;
   d.act_cap = s.act_cap > 0.0f ? s.act_cap : INFINITY;
-  d.head_scale = quant ? act_scales[2 * NB] : 1.0f;
+  d.head_scale = hs;
   d.stem_w = at(0);
   d.tower_w = at(1);
   d.head_w = at(2);
@@ -361,6 +383,9 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   d.fc1_w = reinterpret_cast<const float*>(at(8));
   d.fc1_b = reinterpret_cast<const float*>(at(9));
   d.fc2_w = reinterpret_cast<const float*>(at(10));
+  d.head_sc = reinterpret_cast<const float*>(at(11));
+  d.head_bc = reinterpret_cast<const float*>(at(12));
+  d.fc1_t = reinterpret_cast<const float*>(at(13));
   d.fc2_b = v.fc2_b[0];
   *out = net;
   return AZ_OK;
