@@ -40,8 +40,8 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_37447_amd", "csrc", "az_kernels_mfma
 # for the kernel source it was taken on only: any other source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {  # (workload, tiling): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    ("net20x128_int8_b1024", 3): ("2a8deb25cf03b496a3a2d1ea95606759ffd2105efa95b55ffde0db91f9ac14c4",
-                                  29536.6, 18704.0),
+    ("net20x128_int8_b1024", 3): ("b9bd3d55db80720f503d375e8be1c48f5f2e42261548b86b1ec53f53c647a5e2",
+                                  32097.4, 18704.0),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
