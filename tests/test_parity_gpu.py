@@ -243,3 +243,69 @@ def test_eval_argument_errors_on_device():
         assert az.az_net_tiling_for(net, 1024) == 1 and az.az_net_tiling_for(net, 32) == 2  # bf16
     finally:
         az.az_net_free(net)
+
+
+# --------------------------------------------------------------------------- #
+# Shapes and options across the MFMA kernels: filter widths 64 / 128 / 256,
+# plane, policy and hidden counts away from the workloads', the capped
+# activation and the value-conv ReLU, and the fixed-scale ReLU6 int8 recipe
+# (the capped activation of Section 4.3 lets every activation scale be cap/127)
+# --------------------------------------------------------------------------- #
+_SHAPE_CASES = [
+    # name, NetShape kwargs, dtype, activation-scale mode
+    ("f64_bf16_cap6_vrelu", dict(in_planes=20, blocks=3, filters=64, policy_planes=73, value_hidden=64,
+                                 value_conv_relu=1, act_cap=6.0), "bf16", None),
+    ("f64_int8", dict(in_planes=20, blocks=3, filters=64, policy_planes=73, value_hidden=128), "int8", "absmax"),
+    ("f64_fp8_cap6", dict(in_planes=20, blocks=3, filters=64, policy_planes=73, value_hidden=128, act_cap=6.0),
+     "fp8", "absmax"),
+    ("f128_int8_relu6_fixed", dict(in_planes=20, blocks=4, filters=128, policy_planes=73, value_hidden=128,
+                                   act_cap=6.0), "int8", "fixed"),
+    ("f128_bf16_c32_p1_h512", dict(in_planes=32, blocks=2, filters=128, policy_planes=1, value_hidden=512),
+     "bf16", None),
+    ("f128_bf16_c7_p95_h100_vrelu", dict(in_planes=7, blocks=2, filters=128, policy_planes=95, value_hidden=100,
+                                         value_conv_relu=1), "bf16", None),
+    ("f128_fp8_c12_p40", dict(in_planes=12, blocks=2, filters=128, policy_planes=40, value_hidden=64), "fp8",
+     "absmax"),
+    ("f256_int8_cap6", dict(in_planes=20, blocks=2, filters=256, policy_planes=73, value_hidden=128,
+                            act_cap=6.0), "int8", "absmax"),
+    ("f256_fp8", dict(in_planes=20, blocks=2, filters=256, policy_planes=73, value_hidden=128), "fp8", "absmax"),
+]
+
+
+def _shape_inputs(shape, n, seed):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    planes = (rng.random((n, shape.in_planes, 8, 8)) < 0.3).astype(np.float32)
+    legal = np.zeros((n, shape.n_moves), dtype=np.uint8)
+    for i in range(n):
+        k = int(rng.integers(1, min(40, shape.n_moves) + 1))
+        legal[i, rng.choice(shape.n_moves, size=k, replace=False)] = 1
+    legal[0] = 0          # terminal row
+    legal[1] = 1          # every cell legal
+    return planes, legal
+
+
+@pytest.mark.parametrize("name,kw,dtype,scales", _SHAPE_CASES, ids=[c[0] for c in _SHAPE_CASES])
+def test_shape_and_option_parity(name, kw, dtype, scales):
+    shape = azgen.NetShape(**kw)
+    blob = azgen.make_weights(shape, 700 + len(name), alpha_fold=True, bf16=True)
+    _scale_fc2(shape, blob, 1.0 / 8)   # keep tanh off saturation so |dV| measures the network
+    ws = acs = None
+    if scales == "absmax":
+        calib, _ = _shape_inputs(shape, 64, 99)
+        ws = O.weight_scales(shape, blob, dtype)
+        acs = O.act_scales_from_absmax(O.calibrate_absmax(shape, blob, calib), dtype)
+    elif scales == "fixed":
+        ws = O.weight_scales(shape, blob, dtype)
+        acs = np.full(shape.n_act_scales(), np.float32(shape.act_cap / 127.0), dtype=np.float32)
+    planes, legal = _shape_inputs(shape, 21, 5)
+    tilings = (1, 2) if shape.filters == 256 else (1, 2, 3)
+    _print(f"case shape {name} {dtype} B=21 tilings {tilings}")
+    outs = [H.gpu_eval(shape, blob, dtype, planes, legal, ws, acs, tiling=t) for t in tilings]
+    for P, V in outs[1:]:
+        assert np.array_equal(P, outs[0][0]) and np.array_equal(V, outs[0][1])
+    Pg, Vg = outs[0]
+    H.assert_policy_structure(Pg, legal)
+    assert np.all(Pg[0] == 0.0)
+    Pr, Vr = H.oracle_eval(shape, blob, dtype, planes, legal, ws, acs)
+    dp, dv = H.compare(Pg, Vg, Pr, Vr, dtype)
+    _print(f"  |dP| {dp:.3g} |dV| {dv:.3g}")
