@@ -261,17 +261,32 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // ---- ingest: zero row, planes -> bf16 [board][square][32 channels] at OFF_T
   for (int i = tid; i < C::ZB / 16; i += NT)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
-  // one item = 4 squares of one (board, input plane): a 16-byte load, four bf16 stores
-  for (int idx = tid; idx < BPW * 32 * 16; idx += NT) {
-    const int q4 = idx & 15, c = (idx >> 4) & 31, bl = idx >> 9, b = b0 + bl;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (b < B && c < Cin) v = *reinterpret_cast<const float4*>(planes + ((size_t)b * Cin + c) * 64 + q4 * 4);
-    const float vv[4] = {v.x, v.y, v.z, v.w};
+  // One item = 8 input planes of one board: lane = square, eight plane loads (each
+  // coalesced over the wave), one 16-byte LDS store.  Items are wave-uniform and
+  // every load is issued before the first is used.
+  {
+    constexpr int ITEMS = BPW * 4, PER = (ITEMS + NW - 1) / NW;
+    float pv[PER][8];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int sq = q4 * 4 + r;
-      *reinterpret_cast<unsigned short*>(smem + OFF_T + (bl * 64 + sq) * 64 + (((c >> 3) ^ swz<64>(sq)) << 4) +
-                                         (c & 7) * 2) = (unsigned short)bf16_bits(vv[r]);
+    for (int it = 0; it < PER; ++it) {
+      const int item = w + it * NW, bl = item >> 2, k = item & 3, b = b0 + bl;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        // unconditional load (clamped to plane 0 of board 0) so that no branch
+        // separates a load from the next one
+        const int c = 8 * k + t;
+        const bool ok = item < ITEMS && b < B && c < Cin;
+        const float x = planes[ok ? ((size_t)b * Cin + c) * 64 + lane : (size_t)lane];
+        pv[it][t] = ok ? x : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int item = w + it * NW, bl = item >> 2, k = item & 3;
+      if (item < ITEMS)
+        *reinterpret_cast<uint4*>(smem + OFF_T + (bl * 64 + lane) * 64 + ((k ^ swz<64>(lane)) << 4)) =
+            make_uint4(pack_bf16x2(pv[it][0], pv[it][1]), pack_bf16x2(pv[it][2], pv[it][3]),
+                       pack_bf16x2(pv[it][4], pv[it][5]), pack_bf16x2(pv[it][6], pv[it][7]));
     }
   }
 
@@ -606,8 +621,9 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = 1024 * (spart + WPB * ii) + 256 * u + 4 * lane;
-      mk0[ii][u] = 0u;
-      if (svalid && c < NMV) mk0[ii][u] = *reinterpret_cast<const uint32_t*>(legal + (size_t)sb * NMV + c);
+      const bool ok = svalid && c < NMV;
+      const uint32_t x = *reinterpret_cast<const uint32_t*>(legal + (ok ? (size_t)sb * NMV + c : (size_t)0));
+      mk0[ii][u] = ok ? x : 0u;
     }
   {
     constexpr int HS = F / 16, RBX = C::RBX, OFF_X = C::OFF_X, NBH = C::NBH;
@@ -773,8 +789,9 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       float4 wr[16];
 #pragma unroll
       for (int s4 = 0; s4 < 16; ++s4) wr[s4] = src[(size_t)s4 * H];
-      float g = ok ? p.fc1_b[k] : 0.0f;
-      const float w2 = ok ? p.fc2_w[k] : 0.0f;
+      const float gb = p.fc1_b[ok ? k : 0], w2r = p.fc2_w[ok ? k : 0];
+      float g = ok ? gb : 0.0f;
+      const float w2 = ok ? w2r : 0.0f;
 #pragma unroll
       for (int s4 = 0; s4 < 16; ++s4)
         g += wr[s4].x * u[4 * s4] + wr[s4].y * u[4 * s4 + 1] + wr[s4].z * u[4 * s4 + 2] + wr[s4].w * u[4 * s4 + 3];
