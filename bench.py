@@ -127,6 +127,7 @@ def main():
     ap.add_argument("--tiling", type=int, default=0, choices=(0, 1, 2, 3))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay measurement")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -157,8 +158,11 @@ def main():
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
 
+    def step_on(stream_handle):
+        az.az_eval_batch(net, pl.data_ptr(), lg.data_ptr(), B, pol.data_ptr(), val.data_ptr(), stream_handle)
+
     def step():
-        az.az_eval_batch(net, pl.data_ptr(), lg.data_ptr(), B, pol.data_ptr(), val.data_ptr(), sp)
+        step_on(sp)
 
     for _ in range(args.warmup):
         step()
@@ -176,6 +180,42 @@ def main():
     # sanity: every policy row sums to one, values in range
     s = pol.sum(dim=1)
     ok = bool(((s - 1).abs() < 1e-3).all()) and bool((val.abs() <= 1).all())
+
+    # Outside the timed region: per-call device time (each call between its own
+    # events) and the replay time of the call captured in a HIP graph.
+    pairs = []
+    for _ in range(min(args.steps, 100)):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step()
+        b.record(stream)
+        pairs.append((a, b))
+    torch.cuda.synchronize()
+    lat = np.array([a.elapsed_time(b) * 1000.0 for a, b in pairs])
+    graph_us = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step_on(torch.cuda.current_stream().cuda_stream)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step_on(torch.cuda.current_stream().cuda_stream)
+        g.replay()
+        torch.cuda.synchronize()
+        n_rep = min(args.steps, 100)
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(n_rep):
+            g.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) * 1000.0 / n_rep
+        del g
     az.az_net_free(net)
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)
@@ -200,6 +240,9 @@ def main():
         "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": traffic_bytes(w.name, tiling), "traffic_unit": "bytes per launch"},
+        "latency_us": {"p10": float(np.percentile(lat, 10)), "p50": float(np.percentile(lat, 50)),
+                       "p90": float(np.percentile(lat, 90)), "calls": int(lat.size)},
+        "graph_replay_us": graph_us,
         "outputs_valid": ok,
         "wall_s_timed": wall,
     }

@@ -309,3 +309,48 @@ def test_shape_and_option_parity(name, kw, dtype, scales):
     Pr, Vr = H.oracle_eval(shape, blob, dtype, planes, legal, ws, acs)
     dp, dv = H.compare(Pg, Vg, Pr, Vr, dtype)
     _print(f"  |dP| {dp:.3g} |dV| {dv:.3g}")
+
+
+def test_graph_capture_replays_match_eager():
+    # az_eval_batch allocates nothing and never synchronises, so it can be
+    # captured into a HIP graph; every replay must reproduce the eager result,
+    # with eager work and synchronisations between the replays.
+    import torch
+
+    import paper_2609_37447_amd as az
+    w = W["net20x128_int8_b1024"]
+    blob = azgen.workload_weights(w)
+    ws, acs = H.quant_scales(w.name, "int8")
+    planes, legal = azgen.make_inputs(w, n=64, seed=21)
+    _print("case graph capture int8 B=64")
+    net = az.az_net_load(az.spec_from_shape(w.shape, 64), blob, "int8", ws, acs)
+    try:
+        dev = torch.device("cuda:0")
+        pl = torch.from_numpy(planes).to(dev)
+        lg = torch.from_numpy(legal).to(dev)
+        pol = torch.full((64, w.shape.n_moves), float("nan"), device=dev)
+        val = torch.full((64,), float("nan"), device=dev)
+        az.eval_tensors(net, pl, lg, pol, val)
+        torch.cuda.synchronize()
+        P0, V0 = pol.cpu().clone(), val.cpu().clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            az.eval_tensors(net, pl, lg, pol, val)   # warm-up on the capture stream
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            az.eval_tensors(net, pl, lg, pol, val)
+        for r in range(4):
+            pol.fill_(float("nan"))
+            val.fill_(float("nan"))
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(pol.cpu(), P0) and torch.equal(val.cpu(), V0), f"replay {r}"
+            az.eval_tensors(net, pl, lg, pol, val)    # eager work between replays
+            torch.cuda.synchronize()
+        del g
+    finally:
+        az.az_net_free(net)
