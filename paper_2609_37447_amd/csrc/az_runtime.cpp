@@ -286,14 +286,30 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
     for (int k = 0; k < H; ++k)
       for (int c = 0; c < 64; ++c) fc1t[((size_t)(c / 4) * H + k) * 4 + (c % 4)] = v.fc1_w[(size_t)k * 64 + c];
     if (dtype == AZ_F32) {
-      stem.resize((size_t)F * Cin * 9 * 4);
-      memcpy(stem.data(), v.stem_w, stem.size());
-      tower.resize((size_t)2 * NB * F * F * 9 * 4);
-      for (int n = 0; n < 2 * NB; ++n)
-        memcpy(tower.data() + (size_t)n * F * F * 9 * 4, v.w[n], (size_t)F * F * 9 * 4);
-      head.resize((size_t)(P + 1) * F * 4);
-      memcpy(head.data(), v.pol_w, (size_t)P * F * 4);
-      memcpy(head.data() + (size_t)P * F * 4, v.val_w, (size_t)F * 4);
+      // fp32 kernel: convs as [F/8][C][9][8] and heads as [ceil((P+1)/8)][F][8], so
+      // that the eight output channels (rows) a thread accumulates at one (input
+      // channel, tap) are one contiguous 32-byte load
+      auto pack8 = [](const float* W, int Fo, int C, std::vector<uint8_t>& out) {
+        const size_t base = out.size();
+        out.resize(base + (size_t)Fo * C * 9 * 4);
+        float* o = reinterpret_cast<float*>(out.data() + base);
+        for (int fb = 0; fb < Fo / 8; ++fb)
+          for (int c = 0; c < C; ++c)
+            for (int t = 0; t < 9; ++t)
+              for (int j = 0; j < 8; ++j)
+                o[(((size_t)fb * C + c) * 9 + t) * 8 + j] = W[((size_t)(fb * 8 + j) * C + c) * 9 + t];
+      };
+      pack8(v.stem_w, F, Cin, stem);
+      for (int n = 0; n < 2 * NB; ++n) pack8(v.w[n], F, F, tower);
+      const int RB8 = (P + 1 + 7) / 8;
+      head.assign((size_t)RB8 * F * 8 * 4, 0);
+      float* h = reinterpret_cast<float*>(head.data());
+      for (int rb = 0; rb < RB8; ++rb)
+        for (int f = 0; f < F; ++f)
+          for (int j = 0; j < 8; ++j) {
+            const int row = rb * 8 + j;
+            h[((size_t)rb * F + f) * 8 + j] = row < P ? v.pol_w[(size_t)row * F + f] : row == P ? v.val_w[f] : 0.0f;
+          }
     } else {
       pack_conv(v.stem_w, nullptr, F, Cin, 32, K_BF16, stem);
       const Kind kind = dtype == AZ_BF16 ? K_BF16 : dtype == AZ_INT8 ? K_I8 : K_F8;

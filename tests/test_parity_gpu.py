@@ -354,3 +354,19 @@ def test_graph_capture_replays_match_eager():
         del g
     finally:
         az.az_net_free(net)
+
+
+@pytest.mark.parametrize("filters,blocks", [(64, 2), (256, 1)])
+def test_f32_wide_networks(filters, blocks):
+    # wider fp32 nets: the convolution weights no longer fit the LDS staging area
+    # (global-memory path), and at 256 filters the LDS budget is at its largest
+    shape = azgen.NetShape(in_planes=20, blocks=blocks, filters=filters, policy_planes=73, value_hidden=64,
+                           act_cap=6.0, value_conv_relu=1)
+    blob = azgen.make_weights(shape, 880 + filters, alpha_fold=True, bf16=False)
+    _scale_fc2(shape, blob, 1.0 / 8)
+    planes, legal = _shape_inputs(shape, 9, 6)
+    _print(f"case f32 F={filters} blocks={blocks} B=9")
+    Pg, Vg = H.gpu_eval(shape, blob, "f32", planes, legal)
+    H.assert_policy_structure(Pg, legal)
+    Pr, Vr = O.forward(shape, blob, planes, legal)
+    H.compare_f32(Pg, Vg, Pr, Vr)
