@@ -170,6 +170,25 @@ size_t az_net_device_bytes(const az_net* net);
  * make sure no evaluation on the handle is still running. */
 void az_net_free(az_net* net);
 
+/* Deployment validation (the checks the paper applies to its deployed engine
+ * after every refit, Section "Prediction drift under TensorRT refitting"):
+ * compares two evaluations of the same B positions, a test one (for example the
+ * AZ_INT8 network) against a reference one (its float source), and writes per
+ * position row_metrics[b] = { 1 if the top legal move is the same else 0 (the
+ * first index wins ties; a row without legal moves counts as agreeing),
+ * KL(P_ref || P_test) over the legal cells (terms with P_ref = 0 are 0; P_test is
+ * floored at 1e-30 inside the logarithm), |V_ref - V_test| }.
+ *   policy_ref, policy_test  device, [B][n_moves] fp32, 4-byte aligned.
+ *   value_ref, value_test    device, [B] fp32.
+ *   legal                    device, [B][n_moves] bytes, nonzero = legal.
+ *   row_metrics              device, [B][3] fp32 out.
+ * Asynchronous on stream; allocates nothing.  B == 0 returns AZ_OK.  B < 0,
+ * n_moves <= 0, a NULL or misaligned pointer return AZ_ERR_INVALID_ARG; a launch
+ * failure AZ_ERR_DEVICE.  Uses no network handle. */
+int az_compare_outputs(const float* policy_ref, const float* value_ref, const float* policy_test,
+                       const float* value_test, const uint8_t* legal, int32_t B, int32_t n_moves,
+                       float* row_metrics, void* stream);
+
 /* Static description of a status code. */
 const char* az_status_string(int status);
 

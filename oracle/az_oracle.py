@@ -424,3 +424,33 @@ def forward_quant(spec, blob, w_scales, act_scales, fmt, planes, legal, record=N
                 record.append(q)
     h = q.astype(np.float64) * np.float64(a[2 * nb])
     return heads(spec, W, h, legal)
+
+
+# --------------------------------------------------------------------------- #
+# Deployment validation metrics
+# --------------------------------------------------------------------------- #
+P_FLOOR = 1e-30
+
+
+def compare_outputs(P_ref, V_ref, P_test, V_test, legal):
+    """Per-position agreement of a test evaluation with a reference one, the checks
+    applied to a deployed engine against its source network (Section "Prediction
+    drift under TensorRT refitting": top-one legal-move agreement, legal-policy KL
+    divergence, value error).  Returns float64 arrays (top1_equal, kl, dv):
+      top1_equal[b] = 1 if the first maximising legal cell of P_ref[b] equals that of
+                      P_test[b] (1 for a row without legal cells), else 0;
+      kl[b]         = sum over legal cells with P_ref > 0 of
+                      P_ref * (ln P_ref - ln max(P_test, 1e-30));
+      dv[b]         = |V_ref[b] - V_test[b]|."""
+    Pr = np.asarray(P_ref, dtype=np.float64)
+    Pt = np.asarray(P_test, dtype=np.float64)
+    m = np.asarray(legal) != 0
+    ir = np.argmax(np.where(m, Pr, -np.inf), axis=1)
+    it = np.argmax(np.where(m, Pt, -np.inf), axis=1)
+    has = m.any(axis=1)
+    top1 = np.where(has, (ir == it).astype(np.float64), 1.0)
+    use = m & (Pr > 0)
+    terms = np.where(use, Pr * (np.log(np.where(use, Pr, 1.0)) - np.log(np.maximum(Pt, P_FLOOR))), 0.0)
+    kl = terms.sum(axis=1)
+    dv = np.abs(np.asarray(V_ref, dtype=np.float64) - np.asarray(V_test, dtype=np.float64))
+    return top1, kl, dv

@@ -22,8 +22,8 @@ AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_UNSUPPORTED, AZ_ERR_NOMEM, AZ_ERR_DEVICE = 0, 
 
 # Every symbol include/az.h declares.
 EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_net_set_tiling",
-           "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_status_string",
-           "az_last_error")
+           "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_compare_outputs",
+           "az_status_string", "az_last_error")
 
 
 class az_layer_spec(ctypes.Structure):
@@ -63,6 +63,8 @@ def lib():
         L.az_net_tiling_for.argtypes, L.az_net_tiling_for.restype = [P, I32], ctypes.c_int
         L.az_net_device_bytes.argtypes, L.az_net_device_bytes.restype = [P], SZ
         L.az_net_free.argtypes, L.az_net_free.restype = [P], None
+        L.az_compare_outputs.argtypes = [P, P, P, P, P, I32, I32, P, P]
+        L.az_compare_outputs.restype = ctypes.c_int
         L.az_status_string.argtypes, L.az_status_string.restype = [ctypes.c_int], ctypes.c_char_p
         L.az_last_error.argtypes, L.az_last_error.restype = [], ctypes.c_char_p
         _lib = L
@@ -168,3 +170,42 @@ def eval_tensors(net, planes, legal, policy, value, stream=None) -> int:
     s = torch.cuda.current_stream() if stream is None else stream
     return az_eval_batch(net, planes.data_ptr(), legal.data_ptr(), B, policy.data_ptr(),
                          value.data_ptr(), s.cuda_stream)
+
+
+def az_compare_outputs(policy_ref, value_ref, policy_test, value_test, legal, B: int, n_moves: int,
+                       row_metrics, stream) -> int:
+    """Device pointers (ints); per-row {top-1 equal, KL(ref || test), |dV|} into row_metrics."""
+    return _check(lib().az_compare_outputs(policy_ref, value_ref, policy_test, value_test, legal, B,
+                                           n_moves, row_metrics, stream), "az_compare_outputs")
+
+
+def validate(net_test, net_ref, planes, legal, min_top1: float = 0.8, max_kl: float = 0.1,
+             max_dv: float = 0.25, stream=None) -> dict:
+    """Deployment validation of a loaded network against a reference network on the
+    same positions (torch device tensors planes [B][C][8][8] f32 and legal [B][P*64]
+    u8): both are evaluated, the library compares them row by row, and the rows are
+    summarised as the mean top-1 legal-move agreement (over rows with a legal move),
+    the mean legal-policy KL(ref || test) and the largest value error.  The default
+    bounds separate a faithful quantised network from a broken engine (the paper's
+    faulty refit showed KL near 1); callers set their own."""
+    import torch
+    B, NM = legal.shape
+    dev = planes.device
+    out = {}
+    for key, net in (("test", net_test), ("ref", net_ref)):
+        pol = torch.empty((B, NM), device=dev)
+        val = torch.empty((B,), device=dev)
+        eval_tensors(net, planes, legal, pol, val, stream)
+        out[key] = (pol, val)
+    rows = torch.empty((B, 3), device=dev)
+    s = torch.cuda.current_stream() if stream is None else stream
+    az_compare_outputs(out["ref"][0].data_ptr(), out["ref"][1].data_ptr(), out["test"][0].data_ptr(),
+                       out["test"][1].data_ptr(), legal.data_ptr(), B, NM, rows.data_ptr(), s.cuda_stream)
+    s.synchronize()
+    r = rows.cpu().numpy().astype(np.float64)
+    has = (legal != 0).any(dim=1).cpu().numpy().astype(bool)
+    top1 = float(r[has, 0].mean()) if has.any() else 1.0
+    kl = float(r[:, 1].mean())
+    dv = float(r[:, 2].max())
+    return {"top1": top1, "kl": kl, "dv_max": dv, "rows": r,
+            "passed": top1 >= min_top1 and kl <= max_kl and dv <= max_dv}

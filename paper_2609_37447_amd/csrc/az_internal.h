@@ -59,3 +59,5 @@ int az_mfma_boards_per_wg(int filters, int tiling);
 bool az_mfma_tiling_valid(int filters, int tiling);
 // Whether an (dtype, filters) pair has MFMA kernels in this build.
 bool az_mfma_supported(int dtype, int filters);
+// Records `detail` for az_last_error() and returns `status`.
+int az_fail(int status, const char* detail);

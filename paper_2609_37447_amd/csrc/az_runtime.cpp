@@ -211,6 +211,10 @@ int choose_tiling(const az_net* n, int B) {
 
 }  // namespace
 
+// Records the detail of a failure for az_last_error() (used by the other
+// translation units of the library).
+int az_fail(int status, const char* detail) { return fail(status, "%s", detail); }
+
 extern "C" {
 
 size_t az_weight_count(const az_layer_spec* spec) {

@@ -102,3 +102,16 @@ def test_eval_and_free_reject_null_handle():
     az.az_net_free(None)                                     # no-op
     with pytest.raises(az.AzError):
         az.az_eval_batch(None, 0, 0, 4, 0, 0, 0)
+
+
+def test_compare_outputs_rejects_bad_arguments_before_device():
+    L = az.lib()
+    p = ctypes.c_void_p(16)  # never dereferenced: every call below fails validation first
+    assert L.az_compare_outputs(p, p, p, p, p, -1, 4672, p, None) == az.AZ_ERR_INVALID_ARG
+    assert L.az_compare_outputs(p, p, p, p, p, 4, 0, p, None) == az.AZ_ERR_INVALID_ARG
+    assert L.az_compare_outputs(None, p, p, p, p, 4, 4672, p, None) == az.AZ_ERR_INVALID_ARG
+    assert L.az_compare_outputs(p, p, p, p, p, 4, 4672, None, None) == az.AZ_ERR_INVALID_ARG
+    q = ctypes.c_void_p(18)  # misaligned float buffer
+    assert L.az_compare_outputs(q, p, p, p, p, 4, 4672, p, None) == az.AZ_ERR_INVALID_ARG
+    assert b"aligned" in L.az_last_error()
+    assert L.az_compare_outputs(None, None, None, None, None, 0, 4672, None, None) == az.AZ_OK

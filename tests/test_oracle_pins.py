@@ -530,3 +530,28 @@ def test_fp8_hw_sum_exact_without_spread_and_bounded_otherwise():
     ex = O.conv3x3(x, w)
     big = O.conv3x3(np.abs(x), np.abs(w))
     assert np.all(np.abs(hw - ex) <= big * (8 * 2.0 ** -12 + 2.0 ** -20))
+
+
+def test_compare_outputs_hand_cases():
+    # identical evaluations agree exactly
+    rng = np.random.default_rng(0)
+    legal = (rng.random((5, 30)) < 0.3).astype(np.uint8)
+    legal[0] = 0
+    P = rng.random((5, 30)) * legal
+    P /= np.maximum(P.sum(axis=1, keepdims=True), 1e-300)
+    V = rng.uniform(-1, 1, 5)
+    t, k, d = O.compare_outputs(P, V, P, V, legal)
+    assert np.all(t == 1.0) and np.all(k == 0.0) and np.all(d == 0.0)
+    # two legal cells: ref (0.75, 0.25), test (0.5, 0.5); the test tie keeps cell 0
+    lg = np.zeros((1, 4), dtype=np.uint8); lg[0, 1] = lg[0, 3] = 1
+    Pr = np.array([[0.0, 0.75, 0.9, 0.25]])   # cell 2 is illegal: ignored even though large
+    Pt = np.array([[0.0, 0.5, 0.0, 0.5]])
+    t, k, d = O.compare_outputs(Pr, [0.5], Pt, [-0.25], lg)
+    assert t[0] == 1.0
+    assert abs(k[0] - (0.75 * np.log(1.5) + 0.25 * np.log(0.5))) < 1e-15
+    assert d[0] == 0.75
+    # different top move, and a legal move the test policy puts at zero
+    Pt2 = np.array([[0.0, 0.0, 0.0, 1.0]])
+    t, k, d = O.compare_outputs(Pr, [0.0], Pt2, [0.0], lg)
+    assert t[0] == 0.0
+    assert abs(k[0] - (0.75 * (np.log(0.75) - np.log(1e-30)) + 0.25 * np.log(0.25))) < 1e-12

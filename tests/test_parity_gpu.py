@@ -370,3 +370,72 @@ def test_f32_wide_networks(filters, blocks):
     H.assert_policy_structure(Pg, legal)
     Pr, Vr = O.forward(shape, blob, planes, legal)
     H.compare_f32(Pg, Vg, Pr, Vr)
+
+
+# --------------------------------------------------------------------------- #
+# Deployment validation (per-row comparison kernel and the validate() gate)
+# --------------------------------------------------------------------------- #
+def _relu6_net():
+    shape = azgen.NetShape(in_planes=20, blocks=4, filters=128, policy_planes=73, value_hidden=128, act_cap=6.0)
+    blob = azgen.make_weights(shape, 4242, alpha_fold=True, bf16=True)
+    _scale_fc2(shape, blob, 1.0 / 8)
+    ws = O.weight_scales(shape, blob, "int8")
+    acs = np.full(shape.n_act_scales(), np.float32(6.0 / 127.0), dtype=np.float32)
+    return shape, blob, ws, acs
+
+
+def test_compare_kernel_matches_definition():
+    import torch
+
+    import paper_2609_37447_amd as az
+    shape, blob, ws, acs = _relu6_net()
+    planes, legal = _shape_inputs(shape, 40, 8)
+    _print("case compare kernel int8 vs bf16 B=40")
+    Pq, Vq = H.gpu_eval(shape, blob, "int8", planes, legal, ws, acs)
+    Pb, Vb = H.gpu_eval(shape, blob, "bf16", planes, legal)
+    dev = torch.device("cuda:0")
+    t = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+    pr, vr, pt, vt = t(Pb), t(Vb), t(Pq), t(Vq)
+    lg = t(legal, torch.uint8)
+    rows = torch.full((40, 3), float("nan"), device=dev)
+    az.az_compare_outputs(pr.data_ptr(), vr.data_ptr(), pt.data_ptr(), vt.data_ptr(), lg.data_ptr(), 40,
+                          shape.n_moves, rows.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    g = rows.cpu().numpy().astype(np.float64)
+    # the definition, on the same float32 values
+    top1, kl, dv = O.compare_outputs(pr.cpu().numpy(), vr.cpu().numpy(), pt.cpu().numpy(), vt.cpu().numpy(), legal)
+    assert np.array_equal(g[:, 0], top1)
+    assert np.all(np.abs(g[:, 1] - kl) <= 1e-5 + 1e-4 * np.abs(kl)), np.abs(g[:, 1] - kl).max()
+    assert np.all(np.abs(g[:, 2] - dv) <= 1e-7)
+
+
+def test_validate_gate_passes_faithful_and_flags_broken():
+    import torch
+
+    import paper_2609_37447_amd as az
+    shape, blob, ws, acs = _relu6_net()
+    planes, legal = _shape_inputs(shape, 64, 9)
+    dev = torch.device("cuda:0")
+    pl = torch.from_numpy(planes).to(dev)
+    lg = torch.from_numpy(legal).to(dev)
+    spec = az.spec_from_shape(shape, 64)
+    ref = az.az_net_load(spec, blob, "bf16")
+    good = az.az_net_load(spec, blob, "int8", ws, acs)
+    broken = az.az_net_load(spec, blob, "int8", ws, acs * np.float32(0.1))  # mis-scaled activations
+    try:
+        _print("case validate gate")
+        r_good = az.validate(good, ref, pl, lg)
+        r_bad = az.validate(broken, ref, pl, lg)
+        _print(f"  faithful: top1 {r_good['top1']:.3f} KL {r_good['kl']:.4f} |dV| {r_good['dv_max']:.3f}; "
+               f"broken: top1 {r_bad['top1']:.3f} KL {r_bad['kl']:.4f} |dV| {r_bad['dv_max']:.3f}")
+        assert r_good["passed"] and not r_bad["passed"]
+        assert r_bad["kl"] > 10 * r_good["kl"]
+        # the summary is the definition's, over the rows that have a legal move
+        has = legal.any(axis=1)
+        for r in (r_good, r_bad):
+            assert r["rows"].shape == (64, 3)
+            assert abs(r["top1"] - r["rows"][has, 0].mean()) < 1e-12
+            assert abs(r["kl"] - r["rows"][:, 1].mean()) < 1e-12
+    finally:
+        for n in (ref, good, broken):
+            az.az_net_free(n)
