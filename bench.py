@@ -118,6 +118,43 @@ def cpu_baseline(w, blob, ws, acs, planes, legal, budget_s=12.0, chunk=64):
                       + (f" ({w.dtype} quantised network)" if w.dtype in ("int8", "fp8") else "")}
 
 
+def pipeline_rates(az, net, w, planes, legal, B, steps):
+    """Positions/s through az_pipeline: inputs copied from pinned host buffers,
+    evaluation, outputs copied back, batches of B submitted round-robin over the
+    slots.  Measured after the timed region; never the headline value."""
+    spec = az.spec_from_shape(w.shape, B)
+    res = {"batch": B, "graphs": True,
+           "bytes_in_per_batch": int(planes.nbytes + legal.nbytes),
+           "bytes_out_per_batch": int(B * (w.shape.n_moves + 1) * 4)}
+    n = max(8, min(steps, 100))
+    for slots in (1, 4):
+        pipe = az.Pipeline(net, spec, B, slots, True)
+        try:
+            for k in range(slots):
+                pipe.views[k][0][:] = planes
+                pipe.views[k][1][:] = legal
+            for k in range(slots):             # capture each slot's graph
+                pipe.submit(k, B)
+            for k in range(slots):
+                pipe.wait(k)
+            t0 = time.perf_counter()
+            for i in range(n):
+                k = i % slots
+                pipe.wait(k)
+                pipe.submit(k, B)
+            for k in range(slots):
+                pipe.wait(k)
+            dt = time.perf_counter() - t0
+            v = pipe.views[0]
+            has = legal.any(axis=1)
+            assert np.all(np.abs(v[2][has].sum(axis=1) - 1.0) < 1e-3), "pipeline outputs invalid"
+        finally:
+            pipe.close()
+        res[f"slots{slots}_positions_per_s"] = n * B / dt
+        res[f"slots{slots}_us_per_batch"] = dt * 1e6 / n
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,6 +165,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay measurement")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the host-buffer (PCIe-inclusive) pipeline measurement")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -216,6 +255,7 @@ def main():
         torch.cuda.synchronize()
         graph_us = g0.elapsed_time(g1) * 1000.0 / n_rep
         del g
+    pipeline = None if args.no_pipeline else pipeline_rates(az, net, w, planes, legal, B, args.steps)
     az.az_net_free(net)
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)
@@ -243,6 +283,7 @@ def main():
         "latency_us": {"p10": float(np.percentile(lat, 10)), "p50": float(np.percentile(lat, 50)),
                        "p90": float(np.percentile(lat, 90)), "calls": int(lat.size)},
         "graph_replay_us": graph_us,
+        "pipeline_pcie_inclusive": pipeline,
         "outputs_valid": ok,
         "wall_s_timed": wall,
     }

@@ -57,10 +57,11 @@
  *   stem writes q = round_to_code(min(max(fma(acc, inv[0], b[f] * inv[0]), 0),
  *   qhi[0])) from its bf16 accumulation, and the heads take q * a[2*blocks].
  *
- * Threading and streams.  A handle serves one stream at a time: calls on the
- * same handle from different streams may overlap and must be ordered by the
- * caller (load one handle per concurrent stream).  Calls on different handles
- * are independent.  az_last_error() is thread-local.
+ * Threading and streams.  Evaluation only reads a handle (it keeps no
+ * workspace), so az_eval_batch may run concurrently on one handle from several
+ * threads and streams; az_net_set_tiling and az_net_free must not run
+ * concurrently with evaluations on the same handle.  A pipeline (below) is used
+ * by one thread at a time.  az_last_error() is thread-local.
  */
 #ifndef AZ_H
 #define AZ_H
@@ -188,6 +189,51 @@ void az_net_free(az_net* net);
 int az_compare_outputs(const float* policy_ref, const float* value_ref, const float* policy_test,
                        const float* value_test, const uint8_t* legal, int32_t B, int32_t n_moves,
                        float* row_metrics, void* stream);
+
+/* Host submission pipeline (Section 5.2 "Batching and host-side submission":
+ * preallocated staging buffers, asynchronous copies, completion events and graph
+ * replay keep the GPU busy while the host prepares the next batches).  A
+ * pipeline belongs to one loaded handle (which must outlive it) and owns
+ * `slots` independent slots, each with pinned host buffers, device buffers, a
+ * stream and a completion event, sized for max_batch positions.  The caller
+ * writes a slot's inputs into its host buffers, submits it (copy in, evaluate,
+ * copy out, asynchronously on the slot's stream), and reads the outputs from
+ * the slot's host buffers after az_pipeline_wait (or az_pipeline_query returning
+ * AZ_OK).  Slots run independently, so the copies of one overlap the
+ * evaluation of another.  With use_graphs != 0 a slot captures its three steps
+ * into a HIP graph for each new batch size and replays it. */
+typedef struct az_pipeline az_pipeline;
+
+/* Creates a pipeline on the handle's device.  max_batch: 1..the handle's
+ * max_batch; slots: 1..64.  Allocates all buffers (pinned host memory with
+ * hipHostMalloc, device memory, streams, events); nothing leaks on failure.
+ * Returns AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_NOMEM or AZ_ERR_DEVICE. */
+int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t use_graphs,
+                       az_pipeline** out);
+
+/* Host buffers of a slot (any output pointer may be NULL): planes
+ * [max_batch][in_planes][8][8] f32 and legal [max_batch][P*64] u8 (inputs),
+ * policy [max_batch][P*64] f32 and value [max_batch] f32 (outputs).  The
+ * pipeline owns them; they stay valid until az_pipeline_free.  Do not touch a
+ * slot's buffers between its submit and its completion. */
+int az_pipeline_slot(az_pipeline* p, int32_t slot, float** planes, uint8_t** legal, float** policy,
+                     float** value);
+
+/* Submits the first B positions of a slot's inputs (0 <= B <= max_batch) and
+ * returns without waiting.  A slot already in flight returns
+ * AZ_ERR_INVALID_ARG (wait for it first). */
+int az_pipeline_submit(az_pipeline* p, int32_t slot, int32_t B);
+
+/* AZ_OK when the slot's last submission has completed (or nothing is in flight),
+ * 1 while it is still running, or a negative status. */
+int az_pipeline_query(az_pipeline* p, int32_t slot);
+
+/* Blocks until the slot's last submission has completed. */
+int az_pipeline_wait(az_pipeline* p, int32_t slot);
+
+/* Waits for every slot, then frees the pipeline's buffers, streams, events and
+ * graphs; NULL is a no-op. */
+void az_pipeline_free(az_pipeline* p);
 
 /* Static description of a status code. */
 const char* az_status_string(int status);

@@ -23,7 +23,8 @@ AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_UNSUPPORTED, AZ_ERR_NOMEM, AZ_ERR_DEVICE = 0, 
 # Every symbol include/az.h declares.
 EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_net_set_tiling",
            "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_compare_outputs",
-           "az_status_string", "az_last_error")
+           "az_pipeline_create", "az_pipeline_slot", "az_pipeline_submit", "az_pipeline_query",
+           "az_pipeline_wait", "az_pipeline_free", "az_status_string", "az_last_error")
 
 
 class az_layer_spec(ctypes.Structure):
@@ -65,6 +66,15 @@ def lib():
         L.az_net_free.argtypes, L.az_net_free.restype = [P], None
         L.az_compare_outputs.argtypes = [P, P, P, P, P, I32, I32, P, P]
         L.az_compare_outputs.restype = ctypes.c_int
+        L.az_pipeline_create.argtypes = [P, I32, I32, I32, ctypes.POINTER(P)]
+        L.az_pipeline_create.restype = ctypes.c_int
+        L.az_pipeline_slot.argtypes = [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P),
+                                       ctypes.POINTER(P)]
+        L.az_pipeline_slot.restype = ctypes.c_int
+        L.az_pipeline_submit.argtypes, L.az_pipeline_submit.restype = [P, I32, I32], ctypes.c_int
+        L.az_pipeline_query.argtypes, L.az_pipeline_query.restype = [P, I32], ctypes.c_int
+        L.az_pipeline_wait.argtypes, L.az_pipeline_wait.restype = [P, I32], ctypes.c_int
+        L.az_pipeline_free.argtypes, L.az_pipeline_free.restype = [P], None
         L.az_status_string.argtypes, L.az_status_string.restype = [ctypes.c_int], ctypes.c_char_p
         L.az_last_error.argtypes, L.az_last_error.restype = [], ctypes.c_char_p
         _lib = L
@@ -209,3 +219,66 @@ def validate(net_test, net_ref, planes, legal, min_top1: float = 0.8, max_kl: fl
     dv = float(r[:, 2].max())
     return {"top1": top1, "kl": kl, "dv_max": dv, "rows": r,
             "passed": top1 >= min_top1 and kl <= max_kl and dv <= max_dv}
+
+
+def az_pipeline_create(net, max_batch: int, slots: int, use_graphs: bool = True):
+    out = ctypes.c_void_p()
+    _check(lib().az_pipeline_create(net, max_batch, slots, int(bool(use_graphs)), ctypes.byref(out)),
+           "az_pipeline_create")
+    return out
+
+
+def az_pipeline_slot(p, slot: int):
+    """Host pointers (planes, legal, policy, value) of a slot."""
+    ptrs = [ctypes.c_void_p() for _ in range(4)]
+    _check(lib().az_pipeline_slot(p, slot, *[ctypes.byref(x) for x in ptrs]), "az_pipeline_slot")
+    return tuple(x.value for x in ptrs)
+
+
+def az_pipeline_submit(p, slot: int, B: int) -> int:
+    return _check(lib().az_pipeline_submit(p, slot, B), "az_pipeline_submit")
+
+
+def az_pipeline_query(p, slot: int) -> int:
+    return _check(lib().az_pipeline_query(p, slot), "az_pipeline_query")
+
+
+def az_pipeline_wait(p, slot: int) -> int:
+    return _check(lib().az_pipeline_wait(p, slot), "az_pipeline_wait")
+
+
+def az_pipeline_free(p) -> None:
+    lib().az_pipeline_free(p)
+
+
+class Pipeline:
+    """A pipeline with numpy views of its slots' pinned host buffers."""
+
+    def __init__(self, net, spec, max_batch: int, slots: int, use_graphs: bool = True):
+        self.p = az_pipeline_create(net, max_batch, slots, use_graphs)
+        n_moves = spec.policy_planes * 64
+        self.views = []
+        for k in range(slots):
+            pp, lp, po, vp = az_pipeline_slot(self.p, k)
+            f32 = ctypes.POINTER(ctypes.c_float)
+            u8 = ctypes.POINTER(ctypes.c_uint8)
+            self.views.append((
+                np.ctypeslib.as_array(ctypes.cast(pp, f32), (max_batch, spec.in_planes, 8, 8)),
+                np.ctypeslib.as_array(ctypes.cast(lp, u8), (max_batch, n_moves)),
+                np.ctypeslib.as_array(ctypes.cast(po, f32), (max_batch, n_moves)),
+                np.ctypeslib.as_array(ctypes.cast(vp, f32), (max_batch,)),
+            ))
+
+    def submit(self, slot: int, B: int) -> None:
+        az_pipeline_submit(self.p, slot, B)
+
+    def wait(self, slot: int) -> None:
+        az_pipeline_wait(self.p, slot)
+
+    def query(self, slot: int) -> bool:
+        return az_pipeline_query(self.p, slot) == 0
+
+    def close(self) -> None:
+        if self.p is not None:
+            az_pipeline_free(self.p)
+            self.p = None

@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "az.h"
+
 // Rows of the fused policy/value head matrix: policy planes, then the value
 // 1x1 conv row, then zero rows up to three 32-row MFMA blocks.
 #define AZ_HEAD_ROWS 96
@@ -61,3 +63,6 @@ bool az_mfma_tiling_valid(int filters, int tiling);
 bool az_mfma_supported(int dtype, int filters);
 // Records `detail` for az_last_error() and returns `status`.
 int az_fail(int status, const char* detail);
+// Spec and device of a loaded handle.
+const az_layer_spec& az_net_spec(const az_net* n);
+int az_net_device(const az_net* n);

@@ -215,6 +215,9 @@ int choose_tiling(const az_net* n, int B) {
 // translation units of the library).
 int az_fail(int status, const char* detail) { return fail(status, "%s", detail); }
 
+const az_layer_spec& az_net_spec(const az_net* n) { return n->spec; }
+int az_net_device(const az_net* n) { return n->device; }
+
 extern "C" {
 
 size_t az_weight_count(const az_layer_spec* spec) {

@@ -115,3 +115,19 @@ def test_compare_outputs_rejects_bad_arguments_before_device():
     assert L.az_compare_outputs(q, p, p, p, p, 4, 4672, p, None) == az.AZ_ERR_INVALID_ARG
     assert b"aligned" in L.az_last_error()
     assert L.az_compare_outputs(None, None, None, None, None, 0, 4672, None, None) == az.AZ_OK
+
+
+def test_pipeline_rejects_bad_arguments_before_device():
+    L = az.lib()
+    out = ctypes.c_void_p()
+    assert L.az_pipeline_create(None, 4, 2, 1, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert out.value is None
+    p = ctypes.c_void_p(16)  # never dereferenced: slot counts are checked first
+    assert L.az_pipeline_create(p, 4, 0, 1, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(p, 4, 65, 1, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(p, 4, 2, 1, None) == az.AZ_ERR_INVALID_ARG
+    for fn in (L.az_pipeline_query, L.az_pipeline_wait):
+        assert fn(None, 0) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_submit(None, 0, 1) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_slot(None, 0, None, None, None, None) == az.AZ_ERR_INVALID_ARG
+    L.az_pipeline_free(None)                                 # no-op
