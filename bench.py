@@ -118,40 +118,70 @@ def cpu_baseline(w, blob, ws, acs, planes, legal, budget_s=12.0, chunk=64):
                       + (f" ({w.dtype} quantised network)" if w.dtype in ("int8", "fp8") else "")}
 
 
-def pipeline_rates(az, net, w, planes, legal, B, steps):
-    """Positions/s through az_pipeline: inputs copied from pinned host buffers,
-    evaluation, outputs copied back, batches of B submitted round-robin over the
-    slots.  Measured after the timed region; never the headline value."""
-    spec = az.spec_from_shape(w.shape, B)
-    res = {"batch": B, "graphs": True,
-           "bytes_in_per_batch": int(planes.nbytes + legal.nbytes),
-           "bytes_out_per_batch": int(B * (w.shape.n_moves + 1) * 4)}
+def pipeline_rates(az, net, w, planes, legal, steps, max_legal=256):
+    """Positions/s through az_pipeline, host buffers to host buffers: inputs
+    copied from pinned memory, evaluation, outputs back in host memory.  Worker
+    threads share one pipeline; each owns some of its slots and keeps them in
+    flight round-robin (wait for the slot, resubmit it).  Three set-ups: dense
+    policy, one worker with four slots of the full batch; the same with the
+    compact legal-move policy; and four workers with two outstanding batches of
+    320 each, compact.  Measured after the timed region; never the headline
+    value."""
+    import threading
+
+    B = w.batch
+    n_moves = w.shape.n_moves
+    res = {"max_legal": max_legal,
+           "bytes_in_per_position": int(planes[0].nbytes + legal[0].nbytes),
+           "bytes_out_per_position_dense": int((n_moves + 1) * 4),
+           "bytes_out_per_position_compact": int((max_legal + 2) * 4)}
     n = max(8, min(steps, 100))
-    for slots in (1, 4):
-        pipe = az.Pipeline(net, spec, B, slots, True)
+    has = legal.any(axis=1)
+    for name, workers, per_worker, batch, K in (("dense_1w4s_b%d" % B, 1, 4, B, 0),
+                                                ("compact_1w4s_b%d" % B, 1, 4, B, max_legal),
+                                                ("compact_4w2s_b320", 4, 2, min(320, B), max_legal)):
+        slots = workers * per_worker
+        spec = az.spec_from_shape(w.shape, batch)
+        pipe = az.Pipeline(net, spec, batch, slots, False, max_legal=K)
         try:
             for k in range(slots):
-                pipe.views[k][0][:] = planes
-                pipe.views[k][1][:] = legal
-            for k in range(slots):             # capture each slot's graph
-                pipe.submit(k, B)
+                pipe.views[k][0][:] = planes[:batch]
+                pipe.views[k][1][:] = legal[:batch]
+                pipe.submit(k, batch)
             for k in range(slots):
                 pipe.wait(k)
+            go = threading.Barrier(workers + 1)
+            errors = []
+
+            def run(mine):
+                go.wait()
+                try:
+                    for i in range(n):
+                        k = mine[i % len(mine)]
+                        pipe.wait(k)
+                        pipe.submit(k, batch)
+                    for k in mine:
+                        pipe.wait(k)
+                except Exception as e:  # reported below
+                    errors.append(e)
+
+            th = [threading.Thread(target=run, args=(list(range(j * per_worker, (j + 1) * per_worker)),))
+                  for j in range(workers)]
+            for t in th:
+                t.start()
+            go.wait()
             t0 = time.perf_counter()
-            for i in range(n):
-                k = i % slots
-                pipe.wait(k)
-                pipe.submit(k, B)
-            for k in range(slots):
-                pipe.wait(k)
+            for t in th:
+                t.join()
             dt = time.perf_counter() - t0
-            v = pipe.views[0]
-            has = legal.any(axis=1)
-            assert np.all(np.abs(v[2][has].sum(axis=1) - 1.0) < 1e-3), "pipeline outputs invalid"
+            if errors:
+                raise errors[0]
+            # every legal move fits in max_legal here, so compact rows sum to one too
+            v = pipe.views[slots - 1]
+            assert np.all(np.abs(v[2][:batch][has[:batch]].sum(axis=1) - 1.0) < 1e-3), "pipeline outputs invalid"
         finally:
             pipe.close()
-        res[f"slots{slots}_positions_per_s"] = n * B / dt
-        res[f"slots{slots}_us_per_batch"] = dt * 1e6 / n
+        res[name] = {"positions_per_s": workers * n * batch / dt, "batches": workers * n}
     return res
 
 
@@ -255,7 +285,7 @@ def main():
         torch.cuda.synchronize()
         graph_us = g0.elapsed_time(g1) * 1000.0 / n_rep
         del g
-    pipeline = None if args.no_pipeline else pipeline_rates(az, net, w, planes, legal, B, args.steps)
+    pipeline = None if args.no_pipeline else pipeline_rates(az, net, w, planes, legal, args.steps)
     az.az_net_free(net)
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)

@@ -199,25 +199,46 @@ int az_compare_outputs(const float* policy_ref, const float* value_ref, const fl
  * writes a slot's inputs into its host buffers, submits it (copy in, evaluate,
  * copy out, asynchronously on the slot's stream), and reads the outputs from
  * the slot's host buffers after az_pipeline_wait (or az_pipeline_query returning
- * AZ_OK).  Slots run independently, so the copies of one overlap the
- * evaluation of another.  With use_graphs != 0 a slot captures its three steps
- * into a HIP graph for each new batch size and replays it. */
+ * AZ_OK).  Without AZ_PIPE_GRAPHS the slots share three in-order streams
+ * (copy-in, compute, copy-out) and run in submission order, so the input
+ * copies of later slots overlap the evaluation of earlier ones.  Several
+ * threads may use one pipeline as long as each slot is used by one thread at a
+ * time (submission is serialised inside).
+ *
+ * Flags:
+ *   AZ_PIPE_GRAPHS          give each slot a stream of its own, capture its
+ *                           steps into a HIP graph for each new batch size and
+ *                           replay it;
+ *   AZ_PIPE_COMPACT_POLICY  return only the legal moves' probabilities: per
+ *                           position, the probabilities of its legal cells in
+ *                           ascending cell index order, in max_legal floats
+ *                           (zero past the last legal move), plus the number of
+ *                           legal cells.  This is what a search node expands;
+ *                           a kernel writes it, with the value, straight into
+ *                           the slot's mapped host buffers, so no output copy
+ *                           is needed. */
+#define AZ_PIPE_GRAPHS 1
+#define AZ_PIPE_COMPACT_POLICY 2
+
 typedef struct az_pipeline az_pipeline;
 
 /* Creates a pipeline on the handle's device.  max_batch: 1..the handle's
- * max_batch; slots: 1..64.  Allocates all buffers (pinned host memory with
- * hipHostMalloc, device memory, streams, events); nothing leaks on failure.
- * Returns AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_NOMEM or AZ_ERR_DEVICE. */
-int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t use_graphs,
+ * max_batch; slots: 1..64; flags: an OR of AZ_PIPE_*; max_legal: 1..P*64 with
+ * AZ_PIPE_COMPACT_POLICY, else 0.  Allocates all buffers (pinned host memory
+ * with hipHostMalloc, device memory, streams, events); nothing leaks on
+ * failure.  Returns AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_NOMEM or AZ_ERR_DEVICE. */
+int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t flags, int32_t max_legal,
                        az_pipeline** out);
 
 /* Host buffers of a slot (any output pointer may be NULL): planes
- * [max_batch][in_planes][8][8] f32 and legal [max_batch][P*64] u8 (inputs),
- * policy [max_batch][P*64] f32 and value [max_batch] f32 (outputs).  The
- * pipeline owns them; they stay valid until az_pipeline_free.  Do not touch a
- * slot's buffers between its submit and its completion. */
+ * [max_batch][in_planes][8][8] f32 and legal [max_batch][P*64] u8 (inputs);
+ * value [max_batch] f32 and policy (outputs): [max_batch][P*64] f32, or with
+ * AZ_PIPE_COMPACT_POLICY [max_batch][max_legal] f32 plus legal_count
+ * [max_batch] i32 (NULL without the flag).  The pipeline owns them; they stay
+ * valid until az_pipeline_free.  Do not touch a slot's buffers between its
+ * submit and its completion. */
 int az_pipeline_slot(az_pipeline* p, int32_t slot, float** planes, uint8_t** legal, float** policy,
-                     float** value);
+                     float** value, int32_t** legal_count);
 
 /* Submits the first B positions of a slot's inputs (0 <= B <= max_batch) and
  * returns without waiting.  A slot already in flight returns
@@ -225,10 +246,15 @@ int az_pipeline_slot(az_pipeline* p, int32_t slot, float** planes, uint8_t** leg
 int az_pipeline_submit(az_pipeline* p, int32_t slot, int32_t B);
 
 /* AZ_OK when the slot's last submission has completed (or nothing is in flight),
- * 1 while it is still running, or a negative status. */
+ * 1 while it is still running, or a negative status.  With
+ * AZ_PIPE_COMPACT_POLICY, a completed submission in which some position had
+ * more than max_legal legal cells returns AZ_ERR_INVALID_ARG (that row is
+ * truncated to its first max_legal legal cells; legal_count holds the true
+ * count; every other output is valid). */
 int az_pipeline_query(az_pipeline* p, int32_t slot);
 
-/* Blocks until the slot's last submission has completed. */
+/* Blocks until the slot's last submission has completed; same statuses as
+ * az_pipeline_query apart from 1. */
 int az_pipeline_wait(az_pipeline* p, int32_t slot);
 
 /* Waits for every slot, then frees the pipeline's buffers, streams, events and

@@ -10,6 +10,7 @@ from ._binding import (AZ_ABI_VERSION, AZ_BF16, AZ_ERR_DEVICE, AZ_ERR_INVALID_AR
                        az_layer_spec,
                        az_net_device_bytes, az_net_free, az_net_load, az_net_set_tiling,
                        az_net_tiling_for, az_status_string, az_weight_count, eval_tensors, lib,
-                       make_spec, spec_from_shape, validate, Pipeline, az_pipeline_create,
+                       make_spec, spec_from_shape, validate, Pipeline, AZ_PIPE_COMPACT_POLICY, AZ_PIPE_GRAPHS,
+                       az_pipeline_create,
                        az_pipeline_free, az_pipeline_query, az_pipeline_slot, az_pipeline_submit,
                        az_pipeline_wait)

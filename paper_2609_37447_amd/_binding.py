@@ -66,10 +66,10 @@ def lib():
         L.az_net_free.argtypes, L.az_net_free.restype = [P], None
         L.az_compare_outputs.argtypes = [P, P, P, P, P, I32, I32, P, P]
         L.az_compare_outputs.restype = ctypes.c_int
-        L.az_pipeline_create.argtypes = [P, I32, I32, I32, ctypes.POINTER(P)]
+        L.az_pipeline_create.argtypes = [P, I32, I32, I32, I32, ctypes.POINTER(P)]
         L.az_pipeline_create.restype = ctypes.c_int
         L.az_pipeline_slot.argtypes = [P, I32, ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P),
-                                       ctypes.POINTER(P)]
+                                       ctypes.POINTER(P), ctypes.POINTER(P)]
         L.az_pipeline_slot.restype = ctypes.c_int
         L.az_pipeline_submit.argtypes, L.az_pipeline_submit.restype = [P, I32, I32], ctypes.c_int
         L.az_pipeline_query.argtypes, L.az_pipeline_query.restype = [P, I32], ctypes.c_int
@@ -221,16 +221,20 @@ def validate(net_test, net_ref, planes, legal, min_top1: float = 0.8, max_kl: fl
             "passed": top1 >= min_top1 and kl <= max_kl and dv <= max_dv}
 
 
-def az_pipeline_create(net, max_batch: int, slots: int, use_graphs: bool = True):
+AZ_PIPE_GRAPHS = 1
+AZ_PIPE_COMPACT_POLICY = 2
+
+
+def az_pipeline_create(net, max_batch: int, slots: int, flags: int = 0, max_legal: int = 0):
     out = ctypes.c_void_p()
-    _check(lib().az_pipeline_create(net, max_batch, slots, int(bool(use_graphs)), ctypes.byref(out)),
+    _check(lib().az_pipeline_create(net, max_batch, slots, flags, max_legal, ctypes.byref(out)),
            "az_pipeline_create")
     return out
 
 
 def az_pipeline_slot(p, slot: int):
-    """Host pointers (planes, legal, policy, value) of a slot."""
-    ptrs = [ctypes.c_void_p() for _ in range(4)]
+    """Host pointers (planes, legal, policy, value, legal_count) of a slot."""
+    ptrs = [ctypes.c_void_p() for _ in range(5)]
     _check(lib().az_pipeline_slot(p, slot, *[ctypes.byref(x) for x in ptrs]), "az_pipeline_slot")
     return tuple(x.value for x in ptrs)
 
@@ -252,21 +256,26 @@ def az_pipeline_free(p) -> None:
 
 
 class Pipeline:
-    """A pipeline with numpy views of its slots' pinned host buffers."""
+    """A pipeline with numpy views of its slots' pinned host buffers:
+    views[k] = (planes, legal, policy, value, legal_count or None)."""
 
-    def __init__(self, net, spec, max_batch: int, slots: int, use_graphs: bool = True):
-        self.p = az_pipeline_create(net, max_batch, slots, use_graphs)
+    def __init__(self, net, spec, max_batch: int, slots: int, use_graphs: bool = False,
+                 max_legal: int = 0):
+        flags = (AZ_PIPE_GRAPHS if use_graphs else 0) | (AZ_PIPE_COMPACT_POLICY if max_legal else 0)
+        self.p = az_pipeline_create(net, max_batch, slots, flags, max_legal)
         n_moves = spec.policy_planes * 64
+        f32 = ctypes.POINTER(ctypes.c_float)
+        u8 = ctypes.POINTER(ctypes.c_uint8)
+        i32 = ctypes.POINTER(ctypes.c_int32)
         self.views = []
         for k in range(slots):
-            pp, lp, po, vp = az_pipeline_slot(self.p, k)
-            f32 = ctypes.POINTER(ctypes.c_float)
-            u8 = ctypes.POINTER(ctypes.c_uint8)
+            pp, lp, po, vp, cp = az_pipeline_slot(self.p, k)
             self.views.append((
                 np.ctypeslib.as_array(ctypes.cast(pp, f32), (max_batch, spec.in_planes, 8, 8)),
                 np.ctypeslib.as_array(ctypes.cast(lp, u8), (max_batch, n_moves)),
-                np.ctypeslib.as_array(ctypes.cast(po, f32), (max_batch, n_moves)),
+                np.ctypeslib.as_array(ctypes.cast(po, f32), (max_batch, max_legal or n_moves)),
                 np.ctypeslib.as_array(ctypes.cast(vp, f32), (max_batch,)),
+                np.ctypeslib.as_array(ctypes.cast(cp, i32), (max_batch,)) if max_legal else None,
             ))
 
     def submit(self, slot: int, B: int) -> None:

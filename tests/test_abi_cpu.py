@@ -120,14 +120,20 @@ def test_compare_outputs_rejects_bad_arguments_before_device():
 def test_pipeline_rejects_bad_arguments_before_device():
     L = az.lib()
     out = ctypes.c_void_p()
-    assert L.az_pipeline_create(None, 4, 2, 1, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(None, 4, 2, 0, 0, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
     assert out.value is None
-    p = ctypes.c_void_p(16)  # never dereferenced: slot counts are checked first
-    assert L.az_pipeline_create(p, 4, 0, 1, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
-    assert L.az_pipeline_create(p, 4, 65, 1, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
-    assert L.az_pipeline_create(p, 4, 2, 1, None) == az.AZ_ERR_INVALID_ARG
+    p = ctypes.c_void_p(16)  # never dereferenced: slots, flags and max_legal are checked first
+    assert L.az_pipeline_create(p, 4, 0, 0, 0, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(p, 4, 65, 0, 0, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(p, 4, 2, 0, 0, None) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(p, 4, 2, 8, 0, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert b"flags" in L.az_last_error()
+    compact = az.AZ_PIPE_COMPACT_POLICY
+    assert L.az_pipeline_create(p, 4, 2, compact, 0, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_create(p, 4, 2, 0, 64, ctypes.byref(out)) == az.AZ_ERR_INVALID_ARG
+    assert b"max_legal" in L.az_last_error()
     for fn in (L.az_pipeline_query, L.az_pipeline_wait):
         assert fn(None, 0) == az.AZ_ERR_INVALID_ARG
     assert L.az_pipeline_submit(None, 0, 1) == az.AZ_ERR_INVALID_ARG
-    assert L.az_pipeline_slot(None, 0, None, None, None, None) == az.AZ_ERR_INVALID_ARG
+    assert L.az_pipeline_slot(None, 0, None, None, None, None, None) == az.AZ_ERR_INVALID_ARG
     L.az_pipeline_free(None)                                 # no-op

@@ -33,6 +33,7 @@ def test_pipeline_matches_eval_batch(wname, dtype, use_graphs):
     pipe = None
     try:
         pipe = az.Pipeline(net, spec, MB, SLOTS, use_graphs)
+        assert pipe.views[0][4] is None
         dev = torch.device("cuda:0")
         # batch sizes per round and slot: full, ragged, one, empty, a repeat of
         # an earlier size (graph reuse) and a change back (recapture)
@@ -41,7 +42,7 @@ def test_pipeline_matches_eval_batch(wname, dtype, use_graphs):
             want = []
             for k, B in enumerate(sizes):
                 planes, legal = azgen.make_inputs(w, n=max(B, 1), seed=100 + 10 * r + k)
-                pl, lg, po, va = pipe.views[k]
+                pl, lg, po, va, _ = pipe.views[k]
                 pl[:B] = planes[:B]
                 lg[:B] = legal[:B]
                 po[:] = np.nan
@@ -59,7 +60,7 @@ def test_pipeline_matches_eval_batch(wname, dtype, use_graphs):
                 pipe.wait(k)
                 assert pipe.query(k)
             for k, B in enumerate(sizes):
-                _, _, po, va = pipe.views[k]
+                _, _, po, va, _ = pipe.views[k]
                 assert np.array_equal(po[:B], want[k][0]), f"round {r} slot {k} B={B} policy"
                 assert np.array_equal(va[:B], want[k][1]), f"round {r} slot {k} B={B} value"
                 assert np.all(np.isnan(po[B:])) and np.all(np.isnan(va[B:])), "rows past B written"
@@ -71,6 +72,152 @@ def test_pipeline_matches_eval_batch(wname, dtype, use_graphs):
         pipe.wait(0)
         with pytest.raises(az.AzError):
             pipe.submit(0, 49)
+    finally:
+        if pipe is not None:
+            pipe.close()
+        az.az_net_free(net)
+
+
+def _compact_definition(P, legal, K):
+    """Per row: probabilities of the legal cells in ascending cell order, first K, zero-padded."""
+    out = np.zeros((P.shape[0], K), np.float32)
+    cnt = np.zeros(P.shape[0], np.int32)
+    for r in range(P.shape[0]):
+        v = P[r][legal[r] != 0]
+        cnt[r] = v.size
+        out[r, :min(K, v.size)] = v[:K]
+    return out, cnt
+
+
+@pytest.mark.parametrize("use_graphs", [False, True])
+def test_pipeline_compact_policy(use_graphs):
+    import torch
+
+    import paper_2609_37447_amd as az
+    w = W["net20x128_int8_b1024"]
+    blob = azgen.workload_weights(w)
+    ws, acs = H.quant_scales(w.name, "int8")
+    MB, K = 300, 48
+    _print(f"case pipeline compact int8 graphs={use_graphs} max_batch={MB} max_legal={K}")
+    spec = az.spec_from_shape(w.shape, MB)
+    net = az.az_net_load(spec, blob, "int8", ws, acs)
+    pipe = None
+    try:
+        pipe = az.Pipeline(net, spec, MB, 2, use_graphs, max_legal=K)
+        dev = torch.device("cuda:0")
+        for r, B in enumerate((MB, 257, 1)):
+            planes, legal = azgen.make_inputs(w, n=B, seed=300 + r)
+            if B > 4:
+                legal[0] = 0                          # terminal row: nothing legal
+                legal[1] = 0
+                legal[1, -K:] = 1                     # exactly max_legal, at the end of the row
+                legal[2] = 0
+                legal[2, 5] = 1                       # single legal move
+                legal[3] = 0
+                legal[3, ::97] = 1                    # spread over the row, cut to exactly max_legal
+                legal[3, 97 * K:] = 0
+            k = r % 2
+            pl, lg, po, va, cnt = pipe.views[k]
+            pl[:B] = planes
+            lg[:B] = legal
+            po[:] = np.nan
+            cnt[:] = -1
+            P0 = torch.empty((B, w.shape.n_moves), device=dev)
+            V0 = torch.empty((B,), device=dev)
+            az.eval_tensors(net, torch.from_numpy(planes).to(dev), torch.from_numpy(legal).to(dev), P0, V0)
+            Pd, Vd = P0.cpu().numpy(), V0.cpu().numpy()
+            pipe.submit(k, B)
+            pipe.wait(k)
+            want, wcnt = _compact_definition(Pd, legal, K)
+            assert np.array_equal(cnt[:B], wcnt), f"B={B} counts"
+            assert np.array_equal(po[:B], want), f"B={B} compact policy"
+            assert np.array_equal(va[:B], Vd), f"B={B} value"
+            assert np.all(np.isnan(po[B:])) and np.all(cnt[B:] == -1)
+            _print(f"  B={B} ok (legal counts {wcnt.min()}..{wcnt.max()})")
+        # a row with more legal cells than max_legal: the wait reports it, the row
+        # holds its first K legal probabilities and the true count
+        planes, legal = azgen.make_inputs(w, n=8, seed=399)
+        legal[5, :K + 9] = 1
+        pl, lg, po, va, cnt = pipe.views[0]
+        pl[:8] = planes
+        lg[:8] = legal
+        pipe.submit(0, 8)
+        with pytest.raises(az.AzError, match="more than max_legal"):
+            pipe.wait(0)
+        P0 = torch.empty((8, w.shape.n_moves), device=dev)
+        V0 = torch.empty((8,), device=dev)
+        az.eval_tensors(net, torch.from_numpy(planes).to(dev), torch.from_numpy(legal).to(dev), P0, V0)
+        want, wcnt = _compact_definition(P0.cpu().numpy(), legal, K)
+        assert cnt[5] == K + 9 + np.count_nonzero(legal[5, K + 9:])
+        assert np.array_equal(cnt[:8], wcnt) and np.array_equal(po[:8], want)
+        pipe.submit(0, 8)                             # the slot is usable again
+        with pytest.raises(az.AzError):
+            pipe.wait(0)
+    finally:
+        if pipe is not None:
+            pipe.close()
+        az.az_net_free(net)
+
+
+def test_pipeline_worker_threads_share_one_pipeline():
+    # four threads, two slots each, submitting concurrently into one pipeline
+    import threading
+
+    import torch
+
+    import paper_2609_37447_amd as az
+    w = W["net20x128_int8_b1024"]
+    blob = azgen.workload_weights(w)
+    ws, acs = H.quant_scales(w.name, "int8")
+    MB, K, WORKERS, ROUNDS = 96, 64, 4, 3
+    _print(f"case pipeline threads int8 workers={WORKERS} max_batch={MB} max_legal={K}")
+    spec = az.spec_from_shape(w.shape, MB)
+    net = az.az_net_load(spec, blob, "int8", ws, acs)
+    pipe = None
+    try:
+        pipe = az.Pipeline(net, spec, MB, 2 * WORKERS, False, max_legal=K)
+        dev = torch.device("cuda:0")
+        # per slot and round: inputs and the expected compact outputs
+        jobs = {}
+        for k in range(2 * WORKERS):
+            for r in range(ROUNDS):
+                B = MB - 7 * k - r
+                planes, legal = azgen.make_inputs(w, n=B, seed=500 + 10 * k + r)
+                P0 = torch.empty((B, w.shape.n_moves), device=dev)
+                V0 = torch.empty((B,), device=dev)
+                az.eval_tensors(net, torch.from_numpy(planes).to(dev), torch.from_numpy(legal).to(dev), P0, V0)
+                want, wcnt = _compact_definition(P0.cpu().numpy(), legal, K)
+                jobs[k, r] = (planes, legal, want, wcnt, V0.cpu().numpy())
+        torch.cuda.synchronize()
+        errors = []
+
+        def run(mine):
+            try:
+                for r in range(ROUNDS):
+                    for k in mine:
+                        planes, legal = jobs[k, r][:2]
+                        B = planes.shape[0]
+                        pipe.views[k][0][:B] = planes
+                        pipe.views[k][1][:B] = legal
+                        pipe.submit(k, B)
+                    for k in mine:
+                        pipe.wait(k)
+                        _, _, want, wcnt, V = jobs[k, r]
+                        B = want.shape[0]
+                        _, _, po, va, cnt = pipe.views[k]
+                        assert np.array_equal(cnt[:B], wcnt), f"slot {k} round {r} counts"
+                        assert np.array_equal(po[:B], want), f"slot {k} round {r} policy"
+                        assert np.array_equal(va[:B], V), f"slot {k} round {r} value"
+            except Exception as e:  # re-raised in the main thread
+                errors.append(e)
+
+        th = [threading.Thread(target=run, args=([2 * j, 2 * j + 1],)) for j in range(WORKERS)]
+        for t in th:
+            t.start()
+        for t in th:
+            t.join()
+        if errors:
+            raise errors[0]
     finally:
         if pipe is not None:
             pipe.close()
