@@ -26,6 +26,12 @@ engine, on trained weights.  None of those exist here, so:
   the second convolution at export.  For the reduced-precision workloads every
   weight is then rounded to the nearest bfloat16 (ties to even), so that the
   oracle and the GPU library see the same bf16-valued network.
+* the same flag conditions the deployed network's heads: the token embedding
+  (weights and bias) is multiplied by 1/4 and the WDL output layer by 1/8.
+  Drawn literally, the seeded from-to logits have a spread of about 13 (a
+  one-hot policy) and the value saturates at 1; conditioned, the logits have a
+  spread of about 1 and the values are spread over (-1, 1), as a trained
+  network's are.
 
 * the deployed network's 52 planes follow the structure of Table D.1 (see
   make_planes_52), and its legal mask covers the 1,880 from-to actions.
@@ -47,6 +53,10 @@ N_PIECE_PLANES = 12
 
 
 N_FROMTO_ACTIONS = 1880   # 1,792 ray / knight origin-destination pairs + 88 promotions
+
+# conditioning of the deployed network's seeded heads (see the module notes)
+HEAD_EMBED_SCALE = 0.25
+WDL_OUT_SCALE = 0.125
 
 
 @dataclasses.dataclass(frozen=True)
@@ -205,6 +215,10 @@ def make_weights(shape: NetShape, seed: int, alpha_fold: bool, bf16: bool) -> np
             a = rng.standard_normal(shp) * math.sqrt(2.0 / shp[1])
         if ".w2" in name or ".b2" in name:
             a = a * alpha
+        if alpha_fold and name.startswith("embed."):
+            a = a * HEAD_EMBED_SCALE
+        if alpha_fold and shape.value_head == "wdl" and name.startswith("fc2."):
+            a = a * WDL_OUT_SCALE
         parts.append(a.astype(np.float32).ravel())
     blob = np.concatenate(parts)
     if bf16:

@@ -32,7 +32,16 @@ import numpy as np  # noqa: E402
 import azgen  # noqa: E402
 
 CALIB = os.path.join(ROOT, "tests", "golden", "calib_net20x128_seed1004.npz")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_37447_amd", "csrc", "az_kernels_mfma.hip")
+DEPLOYED_SCALES = os.path.join(ROOT, "tests", "golden", "scales_deployed14x160_seed1006.npz")
+CSRC = os.path.join(ROOT, "paper_2609_37447_amd", "csrc")
+
+
+def is_deployed(shape):
+    return getattr(shape, "policy_head", "planes") == "fromto"
+
+
+def kernel_source(shape):
+    return os.path.join(CSRC, "az_kernels_deployed.hip" if is_deployed(shape) else "az_kernels_mfma.hip")
 
 # HBM traffic of the fused kernel from rocprofv3 --pmc passes (FETCH_SIZE, then
 # WRITE_SIZE, KiB per dispatch), scaled by what the same counters read for a plain
@@ -45,17 +54,33 @@ TRAFFIC = {  # (workload, tiling): (sha256 of the kernel source, FETCH_SIZE KiB,
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
-PEAK = {"bf16": 2.5e15, "int8": 5.0e15, "fp8": 5.0e15, "f32_vec": 157.3e12}
+PEAK = {"bf16": 2.5e15, "int8": 5.0e15, "fp8": 5.0e15, "f32_vec": 157.3e12, "f64_vec": 78.6e12}
 
 
 def mac_counts(shape):
-    """Algorithmic multiply-accumulates per position, by layer group (no padding)."""
+    """Algorithmic multiply-accumulates per position, by layer group (no padding,
+    no halo taps, no masked-out logits)."""
     C, F, P, H, NB = shape.in_planes, shape.filters, shape.policy_planes, shape.value_hidden, shape.blocks
+    if not is_deployed(shape):
+        return {
+            "stem": 64 * F * C * 9,
+            "tower": 2 * NB * 64 * F * F * 9,
+            "head_conv": 64 * F * (P + 1),
+            "value_fc": 64 * H + H,
+        }
+    g = F // 4 if shape.pool_every else 0
+    tower, pool_fc = 0, 0
+    for j in range(NB):
+        pool = shape.is_pool_block(j)
+        tower += 64 * F * F * 9 + 64 * F * (F - g if pool else F) * 9
+        pool_fc += (F - g) * 2 * g if pool else 0
+    D, V = shape.token_dim, shape.value_channels
     return {
         "stem": 64 * F * C * 9,
-        "tower": 2 * NB * 64 * F * F * 9,
-        "head_conv": 64 * F * (P + 1),
-        "value_fc": 64 * H + H,
+        "tower": tower,
+        "pool_fc": pool_fc,
+        "head_conv": 64 * (D + V) * F + 2 * 64 * D * D + 64 * 64 * D + 8 * 4 * D,
+        "value_fc": H * V * 64 + 3 * H,
     }
 
 
@@ -64,21 +89,21 @@ def roofline_peak(shape, dtype):
     priced at the unit it runs on."""
     m = mac_counts(shape)
     if dtype == "f32":
-        unit = {"stem": "f32_vec", "tower": "f32_vec", "head_conv": "f32_vec", "value_fc": "f32_vec"}
+        unit = {k: "f32_vec" for k in m}
     else:
         tower = {"bf16": "bf16", "int8": "int8", "fp8": "fp8"}[dtype]
-        unit = {"stem": "bf16", "tower": tower, "head_conv": "bf16", "value_fc": "f32_vec"}
+        unit = {"stem": "bf16", "tower": tower, "head_conv": "bf16", "value_fc": "f32_vec", "pool_fc": "f64_vec"}
     flop = {k: 2.0 * v for k, v in m.items()}
     t_floor = sum(flop[k] / PEAK[unit[k]] for k in flop)
     return sum(flop.values()), sum(flop.values()) / t_floor
 
 
-def traffic_bytes(workload, tiling):
+def traffic_bytes(w, tiling):
     """Scaled HBM bytes per launch, or None without counters for this exact kernel."""
-    e = TRAFFIC.get((workload, tiling))
+    e = TRAFFIC.get((w.name, tiling))
     if e is None:
         return None
-    with open(KERNEL_SRC, "rb") as f:
+    with open(kernel_source(w.shape), "rb") as f:
         if hashlib.sha256(f.read()).hexdigest() != e[0]:
             return None
     return (e[1] * FETCH_SCALE + e[2] * WRITE_SCALE) * 1024.0
@@ -87,6 +112,11 @@ def traffic_bytes(workload, tiling):
 def load_scales(w):
     if w.dtype not in ("int8", "fp8"):
         return None, None
+    if is_deployed(w.shape):
+        if w.name != "deployed14x160_int8_b1024":
+            raise SystemExit(f"no stored scales for workload {w.name}")
+        d = np.load(DEPLOYED_SCALES, allow_pickle=False)
+        return d["w_scales_int8"], d["act_scales_int8"]
     if w.shape != azgen.WORKLOADS["net20x128_int8_b1024"].shape or w.index != 4:
         raise SystemExit(f"no stored calibration for workload {w.name}")
     d = np.load(CALIB, allow_pickle=False)
@@ -99,11 +129,17 @@ def cpu_baseline(w, blob, ws, acs, planes, legal, budget_s=12.0, chunk=64):
     from threadpoolctl import threadpool_info
 
     from oracle import az_oracle as O
+    from oracle import deployed as OD
     done, t0 = 0, time.perf_counter()
     while True:
         s = done % planes.shape[0]
         pl, lg = planes[s:s + chunk], legal[s:s + chunk]
-        if w.dtype in ("int8", "fp8"):
+        if is_deployed(w.shape):
+            if w.dtype == "int8":
+                OD.forward_quant(w.shape, blob, ws, acs, pl, lg)
+            else:
+                OD.forward(w.shape, blob, pl, lg)
+        elif w.dtype in ("int8", "fp8"):
             O.forward_quant(w.shape, blob, ws, acs, w.dtype, pl, lg)
         else:
             O.forward(w.shape, blob, pl, lg)
@@ -306,10 +342,12 @@ def main():
         "config": {"workload": w.name, "blocks": w.shape.blocks, "filters": w.shape.filters,
                    "in_planes": w.shape.in_planes, "policy_planes": w.shape.policy_planes,
                    "value_hidden": w.shape.value_hidden, "batch": B, "tiling": tiling,
+                   "pool_every": w.shape.pool_every, "policy_head": w.shape.policy_head,
+                   "value_head": w.shape.value_head, "n_moves": w.shape.n_moves,
                    "params": w.shape.weight_count(), "flop_per_position": flop_pos},
         "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_bytes(w.name, tiling), "traffic_unit": "bytes per launch"},
+                     "traffic": traffic_bytes(w, tiling), "traffic_unit": "bytes per launch"},
         "latency_us": {"p10": float(np.percentile(lat, 10)), "p50": float(np.percentile(lat, 50)),
                        "p90": float(np.percentile(lat, 90)), "calls": int(lat.size)},
         "graph_replay_us": graph_us,

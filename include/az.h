@@ -57,6 +57,43 @@
  *   stem writes q = round_to_code(min(max(fma(acc, inv[0], b[f] * inv[0]), 0),
  *   qhi[0])) from its bf16 accumulation, and the heads take q * a[2*blocks].
  *
+ * The deployed network (Section 3.5 "Chess representation and outputs",
+ * Section 4.3 "Convolution, attention, and global context", "Three policy
+ * representations", "Value and training-only heads", Appendix D) is selected by
+ * the version-2 spec fields and changes three things:
+ *   global pooling   (pool_every = p > 0) blocks j with j % p == p - 1 split
+ *                    their first convolution's F outputs into Fr = F - F/4
+ *                    regular and g = F/4 pooled channels (the last g):
+ *                      z  = conv3x3(h) + b1
+ *                      pc = act(z[Fr + i]),  i < g
+ *                      gv = [mean over squares of pc_i (i < g), max over squares of pc_i (i < g)]
+ *                      c  = Wg gv                         (Wg is [Fr][2g])
+ *                      t  = act(z[0:Fr] + c)
+ *                      h  = act(h + conv3x3(t) + b2)      (W2 is [F][Fr][3][3])
+ *   from-to policy   (policy_head = AZ_POLICY_FROMTO, token_dim D)
+ *                      tok[s] = relu(We h[:, s] + be),  Q[s] = Wq tok[s] + bq,
+ *                      K[s] = Wk tok[s] + bk,  S[f][t] = Q[f] . K[t] / sqrt(D),
+ *                      O[c][k] = Wp[k] . K[56 + c]
+ *                    over 1,880 actions: the 1,792 origin-destination pairs f -> t
+ *                    on a common row, column or diagonal or a knight's jump apart,
+ *                    ascending (f, t), logit S[f][t]; then the 88 promotions, f on
+ *                    row 6, t on row 7 at most one column away, piece k = 0..3
+ *                    (queen, rook, bishop, knight), ascending (f, t, k), logit
+ *                    S[f][t] + O[t - 56][k].  Squares are row * 8 + column in
+ *                    the side-to-move frame.  The legal-action softmax is the
+ *                    one above, over these 1,880 logits.
+ *   WDL value        (value_head = AZ_VALUE_WDL, value_channels V)
+ *                      u = Wv h + bv (V x 64, then ReLU if value_conv_relu),
+ *                      y = relu(W1 u + b1) (u flattened channel-major),
+ *                      (W, D, L) = softmax(W2 y + b2),  value = W - L.
+ * In AZ_INT8 the pooled channels' mean, maximum and projection are taken in
+ * floating point inside the integer trunk: pc = act(fma(float(acc), a[n] *
+ * s_w[n][f], b1[f])) in fp32, the statistics and Wg gv in fp64, c rounded once to
+ * fp32 and added as z = fma(c, inv[n+1], z) before the regular channels' code
+ * is rounded; the pooled channels are stored as codes like any other output and
+ * read by nothing.  Heads run on bf16 operands with split (hi + lo) products and
+ * fp32 accumulation, softmax and WDL in fp32.
+ *
  * Threading and streams.  Evaluation only reads a handle (it keeps no
  * workspace), so az_eval_batch may run concurrently on one handle from several
  * threads and streams; az_net_set_tiling and az_net_free must not run
@@ -73,7 +110,7 @@
 extern "C" {
 #endif
 
-#define AZ_ABI_VERSION 1
+#define AZ_ABI_VERSION 2
 #define AZ_SQUARES 64
 
 typedef struct az_net az_net; /* opaque: owns the device copy of the packed weights */
@@ -93,29 +130,48 @@ typedef enum {
   AZ_ERR_DEVICE = -4       /* any other HIP runtime failure */
 } az_status;
 
-/* Network shape.  Supported: in_planes 1..32; blocks 1..64; policy_planes
- * 1..95; value_hidden 1..512; act_cap >= 0 (0 = plain ReLU); max_batch
- * 1..1048576.  filters: AZ_F32 any multiple of 8 up to 256; AZ_BF16, AZ_INT8
- * and AZ_FP8_E4M3 one of 64, 128, 256.  Anything else well-formed returns
- * AZ_ERR_UNSUPPORTED. */
+/* Policy and value head kinds (version-2 spec fields). */
+typedef enum { AZ_POLICY_PLANES = 0, AZ_POLICY_FROMTO = 1 } az_policy_head;
+typedef enum { AZ_VALUE_TANH = 0, AZ_VALUE_WDL = 1 } az_value_head;
+#define AZ_FROMTO_ACTIONS 1880
+
+/* Network shape.  abi_version 1 callers pass the first nine fields only (the
+ * move-plane / tanh network); abi_version 2 adds the last five.
+ * Move-plane network (policy_head 0, value_head 0, pool_every 0): in_planes
+ * 1..32; blocks 1..64; policy_planes 1..95; value_hidden 1..512; act_cap >= 0
+ * (0 = plain ReLU); max_batch 1..1048576.  filters: AZ_F32 any multiple of 8
+ * up to 256; AZ_BF16, AZ_INT8 and AZ_FP8_E4M3 one of 64, 128, 256.
+ * Deployed network (policy_head AZ_POLICY_FROMTO with value_head AZ_VALUE_WDL):
+ * AZ_BF16 or AZ_INT8; filters 160; in_planes 1..64; blocks 1..64; policy_planes
+ * 0; token_dim 128; value_channels 1..32; value_hidden 1..512; pool_every >= 0.
+ * Anything else well-formed returns AZ_ERR_UNSUPPORTED. */
 typedef struct {
-  int32_t abi_version;     /* must be AZ_ABI_VERSION */
-  int32_t in_planes;       /* input planes per position (20 in the synthetic encoding) */
+  int32_t abi_version;     /* 1 or 2 (AZ_ABI_VERSION) */
+  int32_t in_planes;       /* input planes per position (20 or 52 in the synthetic encodings) */
   int32_t blocks;          /* residual blocks after the stem */
   int32_t filters;         /* F: channels of the stem and of every block */
-  int32_t policy_planes;   /* P: move-type planes; P*64 policy cells per position */
+  int32_t policy_planes;   /* P: move-type planes; P*64 policy cells per position (0 for from-to) */
   int32_t value_hidden;    /* H: width of the value head's hidden layer */
   int32_t value_conv_relu; /* 0: no activation after the value 1x1 conv; 1: ReLU */
   float act_cap;           /* 0: ReLU; > 0: ReLU capped at act_cap */
   int32_t max_batch;       /* largest B az_eval_batch accepts for this handle */
+  /* abi_version >= 2 */
+  int32_t pool_every;      /* 0: no global pooling; p > 0: blocks j % p == p - 1 pool */
+  int32_t policy_head;     /* az_policy_head */
+  int32_t token_dim;       /* D of the from-to head (0 with the move-plane head) */
+  int32_t value_head;      /* az_value_head */
+  int32_t value_channels;  /* V: 1x1 value channels (1 with the tanh head) */
 } az_layer_spec;
 
 /* Number of floats the canonical weight blob of `spec` must hold, or 0 if the
  * spec is malformed.  Blob order (fp32, PyTorch layouts, concatenated):
  *   stem W[F][in_planes][3][3], b[F];
- *   for each block: W1[F][F][3][3], b1[F], W2[F][F][3][3], b2[F];
- *   policy W[P][F], b[P]; value conv W[1][F], b[1];
- *   fc1 W[H][64], b[H]; fc2 W[1][H], b[1]. */
+ *   for each block: W1[F][F][3][3], b1[F], (pooling blocks: Wg[Fr][2g]),
+ *     W2[F][K][3][3] (K = Fr in pooling blocks, else F), b2[F];
+ *   move-plane head: W[P][F], b[P];  from-to head: We[D][F], be[D], Wq[D][D],
+ *     bq[D], Wk[D][D], bk[D], Wp[4][D];
+ *   tanh value head: W[1][F], b[1], fc1 W[H][64], b[H], fc2 W[1][H], b[1];
+ *   WDL value head: Wv[V][F], bv[V], W1[H][V*64], b1[H], W2[3][H], b2[3]. */
 size_t az_weight_count(const az_layer_spec* spec);
 
 /* Builds a handle on the current HIP device: validates the spec and counts,
@@ -141,15 +197,28 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
  * synchronises, so it can be captured into a HIP graph.
  *   planes  device, [B][in_planes][8][8] fp32, contiguous, 16-byte aligned.
  *           AZ_BF16 / AZ_INT8 / AZ_FP8_E4M3 round the planes to bf16 on entry.
- *   legal   device, [B][P*64] bytes, contiguous, 16-byte aligned; nonzero = legal.
- *   policy  device, [B][P*64] fp32 out, contiguous, 16-byte aligned; every element
+ *   legal   device, [B][n_moves] bytes (n_moves = az_net_moves(net)), contiguous,
+ *           16-byte aligned; nonzero = legal.
+ *   policy  device, [B][n_moves] fp32 out, contiguous, 16-byte aligned; every element
  *           is written; illegal cells are exactly 0.0f.
- *   value   device, [B] fp32 out, in [-1, 1].
+ *   value   device, [B] fp32 out, in [-1, 1] (tanh head: tanh; WDL head: W - L).
  * B == 0 returns AZ_OK and launches nothing.  B < 0, B > max_batch, a NULL or
  * misaligned pointer return AZ_ERR_INVALID_ARG before touching the device.
  * Input values are not checked.  Launch failures return AZ_ERR_DEVICE. */
 int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_t B,
                   float* policy, float* value, void* stream);
+
+/* az_eval_batch with the WDL head's probabilities: wdl, if not NULL, is a
+ * device [B][3] fp32 output (win, draw, loss; 4-byte aligned) and needs a WDL
+ * network (else AZ_ERR_INVALID_ARG).  The policy and legal rows hold
+ * az_net_moves(net) entries.  Same errors and asynchrony as az_eval_batch. */
+int az_eval_batch_wdl(az_net* net, const float* planes, const uint8_t* legal, int32_t B,
+                      float* policy, float* value, float* wdl, void* stream);
+
+/* Policy entries (legal-mask bytes, policy floats) per position: P*64 for the
+ * move-plane head, AZ_FROMTO_ACTIONS for the from-to head; negative status for
+ * a NULL handle. */
+int az_net_moves(const az_net* net);
 
 /* Kernel tiling used by az_eval_batch.  0: chosen from B and the dtype
  * (default); 1 (large): four boards per workgroup (F = 64, 128) or two

@@ -15,13 +15,16 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaz_mi355x.so")
 
-AZ_ABI_VERSION = 1
+AZ_ABI_VERSION = 2
+AZ_POLICY_PLANES, AZ_POLICY_FROMTO = 0, 1
+AZ_VALUE_TANH, AZ_VALUE_WDL = 0, 1
 AZ_F32, AZ_BF16, AZ_INT8, AZ_FP8_E4M3 = 0, 1, 2, 3
 DTYPES = {"f32": AZ_F32, "bf16": AZ_BF16, "int8": AZ_INT8, "fp8": AZ_FP8_E4M3}
 AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_UNSUPPORTED, AZ_ERR_NOMEM, AZ_ERR_DEVICE = 0, -1, -2, -3, -4
 
 # Every symbol include/az.h declares.
-EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_net_set_tiling",
+EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_eval_batch_wdl", "az_net_moves",
+           "az_net_set_tiling",
            "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_compare_outputs",
            "az_pipeline_create", "az_pipeline_slot", "az_pipeline_submit", "az_pipeline_query",
            "az_pipeline_wait", "az_pipeline_free", "az_status_string", "az_last_error")
@@ -32,7 +35,16 @@ class az_layer_spec(ctypes.Structure):
                 ("blocks", ctypes.c_int32), ("filters", ctypes.c_int32),
                 ("policy_planes", ctypes.c_int32), ("value_hidden", ctypes.c_int32),
                 ("value_conv_relu", ctypes.c_int32), ("act_cap", ctypes.c_float),
-                ("max_batch", ctypes.c_int32)]
+                ("max_batch", ctypes.c_int32),
+                # abi_version 2
+                ("pool_every", ctypes.c_int32), ("policy_head", ctypes.c_int32),
+                ("token_dim", ctypes.c_int32), ("value_head", ctypes.c_int32),
+                ("value_channels", ctypes.c_int32)]
+
+
+class az_layer_spec_v1(ctypes.Structure):
+    """The version-1 layout (the first nine fields), as older callers pass it."""
+    _fields_ = az_layer_spec._fields_[:9]
 
 
 class AzError(RuntimeError):
@@ -60,6 +72,9 @@ def lib():
         L.az_net_load.restype = ctypes.c_int
         L.az_eval_batch.argtypes = [P, P, P, I32, P, P, P]
         L.az_eval_batch.restype = ctypes.c_int
+        L.az_eval_batch_wdl.argtypes = [P, P, P, I32, P, P, P, P]
+        L.az_eval_batch_wdl.restype = ctypes.c_int
+        L.az_net_moves.argtypes, L.az_net_moves.restype = [P], ctypes.c_int
         L.az_net_set_tiling.argtypes, L.az_net_set_tiling.restype = [P, I32], ctypes.c_int
         L.az_net_tiling_for.argtypes, L.az_net_tiling_for.restype = [P, I32], ctypes.c_int
         L.az_net_device_bytes.argtypes, L.az_net_device_bytes.restype = [P], SZ
@@ -82,15 +97,25 @@ def lib():
 
 
 def make_spec(in_planes, blocks, filters, policy_planes, value_hidden, value_conv_relu=0,
-              act_cap=0.0, max_batch=1, abi_version=AZ_ABI_VERSION) -> az_layer_spec:
+              act_cap=0.0, max_batch=1, abi_version=AZ_ABI_VERSION, pool_every=0,
+              policy_head=AZ_POLICY_PLANES, token_dim=0, value_head=AZ_VALUE_TANH,
+              value_channels=1) -> az_layer_spec:
     return az_layer_spec(abi_version, in_planes, blocks, filters, policy_planes, value_hidden,
-                         value_conv_relu, act_cap, max_batch)
+                         value_conv_relu, act_cap, max_batch, pool_every, policy_head, token_dim,
+                         value_head, value_channels)
 
 
 def spec_from_shape(shape, max_batch: int) -> az_layer_spec:
     """az_layer_spec from any object with the NetShape attribute names."""
+    fromto = getattr(shape, "policy_head", "planes") == "fromto"
+    wdl = getattr(shape, "value_head", "tanh") == "wdl"
     return make_spec(shape.in_planes, shape.blocks, shape.filters, shape.policy_planes,
-                     shape.value_hidden, shape.value_conv_relu, shape.act_cap, max_batch)
+                     shape.value_hidden, shape.value_conv_relu, shape.act_cap, max_batch,
+                     pool_every=getattr(shape, "pool_every", 0),
+                     policy_head=AZ_POLICY_FROMTO if fromto else AZ_POLICY_PLANES,
+                     token_dim=shape.token_dim if fromto else 0,
+                     value_head=AZ_VALUE_WDL if wdl else AZ_VALUE_TANH,
+                     value_channels=getattr(shape, "value_channels", 1))
 
 
 def _check(status: int, where: str) -> int:
@@ -135,6 +160,16 @@ def az_eval_batch(net, planes_ptr: int, legal_ptr: int, B: int, policy_ptr: int,
     return _check(st, "az_eval_batch") if raise_on_error else st
 
 
+def az_eval_batch_wdl(net, planes_ptr: int, legal_ptr: int, B: int, policy_ptr: int, value_ptr: int,
+                      wdl_ptr, stream: int = 0, raise_on_error: bool = True) -> int:
+    st = lib().az_eval_batch_wdl(net, planes_ptr, legal_ptr, int(B), policy_ptr, value_ptr, wdl_ptr, stream)
+    return _check(st, "az_eval_batch_wdl") if raise_on_error else st
+
+
+def az_net_moves(net) -> int:
+    return _check(lib().az_net_moves(net), "az_net_moves")
+
+
 def az_net_set_tiling(net, tiling: int, raise_on_error: bool = True) -> int:
     st = lib().az_net_set_tiling(net, int(tiling))
     return _check(st, "az_net_set_tiling") if raise_on_error else st
@@ -164,11 +199,15 @@ def az_last_error() -> str:
 # torch convenience: device tensors and streams (PyTorch provides memory and
 # streams only)
 # --------------------------------------------------------------------------- #
-def eval_tensors(net, planes, legal, policy, value, stream=None) -> int:
-    """az_eval_batch on torch CUDA tensors; stream defaults to torch's current one."""
+def eval_tensors(net, planes, legal, policy, value, stream=None, wdl=None) -> int:
+    """az_eval_batch (az_eval_batch_wdl when wdl is given) on torch CUDA tensors;
+    stream defaults to torch's current one."""
     import torch
     B = planes.shape[0]
-    for name, t in (("planes", planes), ("legal", legal), ("policy", policy), ("value", value)):
+    named = [("planes", planes), ("legal", legal), ("policy", policy), ("value", value)]
+    if wdl is not None:
+        named.append(("wdl", wdl))
+    for name, t in named:
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous device tensor")
     if planes.dtype != torch.float32 or legal.dtype != torch.uint8:
@@ -178,6 +217,11 @@ def eval_tensors(net, planes, legal, policy, value, stream=None) -> int:
     if legal.shape[0] != B or policy.shape[0] != B or value.shape[0] != B:
         raise ValueError("batch sizes differ")
     s = torch.cuda.current_stream() if stream is None else stream
+    if wdl is not None:
+        if wdl.dtype != torch.float32 or tuple(wdl.shape) != (B, 3):
+            raise ValueError("wdl must be float32 [B, 3]")
+        return az_eval_batch_wdl(net, planes.data_ptr(), legal.data_ptr(), B, policy.data_ptr(),
+                                 value.data_ptr(), wdl.data_ptr(), s.cuda_stream)
     return az_eval_batch(net, planes.data_ptr(), legal.data_ptr(), B, policy.data_ptr(),
                          value.data_ptr(), s.cuda_stream)
 
@@ -263,7 +307,7 @@ class Pipeline:
                  max_legal: int = 0):
         flags = (AZ_PIPE_GRAPHS if use_graphs else 0) | (AZ_PIPE_COMPACT_POLICY if max_legal else 0)
         self.p = az_pipeline_create(net, max_batch, slots, flags, max_legal)
-        n_moves = spec.policy_planes * 64
+        n_moves = az_net_moves(net)
         f32 = ctypes.POINTER(ctypes.c_float)
         u8 = ctypes.POINTER(ctypes.c_uint8)
         i32 = ctypes.POINTER(ctypes.c_int32)

@@ -47,12 +47,46 @@ struct AzDevNet {
   const float* head_sc;  // [AZ_HEAD_ROWS]
   const float* head_bc;  // [AZ_HEAD_ROWS]
   const float* fc1_t;    // [16][H][4]
+
+  // Deployed network (global pooling, from-to policy head, WDL value head); see
+  // az_kernels_deployed.hip for the fragment orders.
+  int pool_every;      // 0: no pooling blocks
+  int value_channels;  // V
+  const void* emb_w;   // bf16 A fragments, rows: D token rows, V value rows, zeros (AZ_DEP_EMB_ROWS)
+  const void* q_w;     // bf16 A fragments of Wq, K dimension in the token accumulators' order
+  const void* k_w;     // same for Wk
+  const void* p_w;     // bf16 A fragments of Wp (4 rows padded to 32), K in the key accumulators' order
+  const float* emb_sc;     // [AZ_DEP_EMB_ROWS] row scale (value of one unit of h)
+  const float* emb_bc;     // [AZ_DEP_EMB_ROWS] row bias: be, then bv, then zeros
+  const float* q_b;        // [D]
+  const float* k_b;        // [D]
+  const double* pool_wt;   // per pooling block j (in block order): Wg^T as [2g][AZ_DEP_POOL_OPAD] fp64
+  const float* pool_m;     // [2*blocks][F]: pooled-channel pre-activation scale (a[n]*s_w[n][f]; 1 for bf16)
+  const float* pool_b;     // [2*blocks][F]: pooled-channel bias b1 (unscaled)
+  const float* pool_cinv;  // [2*blocks]: factor of c in the regular channels (inv[n+1]; 1 for bf16)
+  const uint32_t* actions; // [AZ_DEP_ACTION_SLOTS]: f*64 + t | (promotion c*4 + k + 1) << 12
+  const float* wdl_fc1_t;  // [V*64][H] (fc1 transposed)
+  const float* wdl_fc1_b;  // [H]
+  const float* wdl_fc2_w;  // [3][H]
+  float wdl_fc2_b[3];
 };
+
+// Deployed network constants: embedding rows (128 token rows + up to 32 value
+// rows), padded pooled-projection outputs, action-table slots.
+#define AZ_DEP_TOKEN 128
+#define AZ_DEP_EMB_ROWS 160
+#define AZ_DEP_POOL_OPAD 128
+#define AZ_DEP_ACTION_SLOTS 2048
+#define AZ_DEP_MAX_IN_PLANES 64
 
 // Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small, 3 = medium.
 hipError_t az_launch_mfma(int dtype, int tiling, const AzDevNet& net, const float* planes,
                           const uint8_t* legal, int B, float* policy, float* value,
                           hipStream_t stream);
+// Deployed network (AZ_BF16 / AZ_INT8, F = 160); wdl may be NULL.
+hipError_t az_launch_deployed(int dtype, const AzDevNet& net, const float* planes,
+                              const uint8_t* legal, int B, float* policy, float* value, float* wdl,
+                              hipStream_t stream);
 hipError_t az_launch_f32(const AzDevNet& net, const float* planes, const uint8_t* legal, int B,
                          float* policy, float* value, hipStream_t stream);
 // Boards per workgroup of a tiling (for grid sizing and tests).
@@ -63,6 +97,8 @@ bool az_mfma_tiling_valid(int filters, int tiling);
 bool az_mfma_supported(int dtype, int filters);
 // Records `detail` for az_last_error() and returns `status`.
 int az_fail(int status, const char* detail);
-// Spec and device of a loaded handle.
+// Spec (normalised to the current version) and device of a loaded handle.
 const az_layer_spec& az_net_spec(const az_net* n);
+// Policy entries per position of a spec: P*64, or AZ_FROMTO_ACTIONS.
+int az_spec_moves(const az_layer_spec& s);
 int az_net_device(const az_net* n);

@@ -1,0 +1,827 @@
+// Fused evaluation of the paper's deployed network on CDNA4 matrix cores
+// (gfx950): 160-channel residual tower with global-pooling blocks, from-to
+// policy head and WDL value head (Section 3.5 "Chess representation and
+// outputs", Section 4.3 "Convolution, attention, and global context", "Three
+// policy representations", "Value and training-only heads", Appendix D).
+//
+// One workgroup is one wave and evaluates one board end to end; four such
+// workgroups share a compute unit (int8), one per SIMD.  The wave owns every
+// output channel (five 32-channel MFMA blocks) and both half-board square
+// blocks of every layer, so global pooling, the heads and both softmaxes need
+// no exchange with other waves.
+//
+// Tower.  Every 3x3 convolution is an implicit GEMM D[ch][sq] = sum_k
+// W[ch][k] X[k][sq], k = tap * C + c, with weights as the A operand (streamed
+// from L2 in pre-packed fragment order through a ring of prefetched K steps)
+// and the board's activations as the B operand, read from LDS rows [square][F
+// channels].  Rows of 160 (int8) or 320 (bf16) bytes are not a power of two,
+// so a row's 16-byte chunks are rotated by a few positions that depend on the
+// square: the 16 lanes of a ds_read_b128 group (16 consecutive squares) then
+// hit 16 different bank groups.  Out-of-board taps read a zero region at the
+// bank slot their virtual square would use.
+//
+// Global pooling (every pool_every-th block).  After the first convolution's
+// K loop, the pooled channels (the last F/4) are activated from the
+// accumulators, their board sum (fp64) and maximum are reduced across the 32
+// lanes of each half-wave, and the projection c = Wg [mean, max] runs in fp64
+// over the wave; c (rounded to fp32) is then added to the regular channels in
+// the same epilogue that writes them.
+//
+// Heads.  The final tensor h (int8 codes, or bf16 hi + lo parts of the fp32
+// residual stream) feeds one bf16 GEMM whose rows are the 128 token rows and
+// the value rows.  The token, query and key products then run from registers:
+// each accumulator tile is split into bf16 hi + lo parts and used directly as
+// an MFMA operand, with the next weight matrix packed in the order the
+// accumulator registers hold their rows (a permutation of the K dimension
+// applied to both operands of the product).  Query-key logits are written to
+// LDS once, gathered through the action table, and soft-maxed over the legal
+// actions in fp32; the WDL head runs on the vector ALUs.
+#include "az_internal.h"
+#include "az_mfma_common.h"
+
+#include <math.h>
+
+namespace {
+
+constexpr int DF = 160;                         // filters
+constexpr int DNMB = DF / 32;                   // 32-channel blocks
+constexpr int DG = DF / 4;                      // pooled channels
+constexpr int DFR = DF - DG;                    // regular channels of a pooling block
+constexpr int DCP = AZ_DEP_MAX_IN_PLANES;       // stem input channels (padded)
+constexpr int DD = AZ_DEP_TOKEN;                // token width
+constexpr int DEMB = AZ_DEP_EMB_ROWS / 32;      // embedding row blocks (tokens + value rows)
+constexpr int DTB = DD / 32;                    // token row blocks
+
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+// Chunk position of logical 16-byte chunk lc in a row of RB bytes at swizzle
+// sw: XOR for rows of 128 bytes, rotation modulo the row's chunk count for the
+// 160- and 320-byte rows.
+template <int RB>
+struct Rot {
+  static constexpr int NC = RB / 16;
+  static constexpr int GC = gcd_c(NC, 16);      // NC*s mod 16 repeats every 16/GC squares
+  static constexpr int SH = GC == 2 ? 3 : GC == 4 ? 2 : 1;
+  static constexpr int RM = GC - 1;
+  static_assert(RB == 160 || RB == 320, "rotated rows");
+  static __device__ __forceinline__ int sw(int sq) { return (sq >> SH) & RM; }
+  static __device__ __forceinline__ int pos(int lc, int sw) {
+    const int x = lc + sw;
+    return x >= NC ? x - NC : x;
+  }
+};
+
+// swizzle of a 128-byte row (the stem's 64 bf16 input channels)
+__device__ __forceinline__ int swz128(int sq) { return (sq >> 1) & 7; }
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// bf16 hi and lo parts of eight fp32 values: x = hi + lo within 2^-16 |x|.
+__device__ __forceinline__ void split8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = x[2 * i], b = x[2 * i + 1];
+    h[i] = pack_bf16x2(a, b);
+    l[i] = pack_bf16x2(a - bf16_round(a), b - bf16_round(b));
+  }
+  hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
+}
+
+__device__ __forceinline__ f32x16 mma_bf16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ double shfl_xor_d(double v, int m) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)u, m), hi = (uint32_t)__shfl_xor((int)(uint32_t)(u >> 32), m);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+template <int MK>
+struct DepCfg {
+  using T = Mk<MK>;
+  static constexpr bool QUANT = MK != MK_BF16;
+  static constexpr int RB = DF * T::ES;               // tower row bytes
+  static constexpr int RBX = 2 * DF;                  // bf16 row bytes of the heads' input
+  static constexpr int BUF = 64 * RB;
+  static constexpr int OFF_H = 0, OFF_T = BUF, OFF_Z = 2 * BUF;
+  static constexpr int ZB = (RB + 256 + 255) / 256 * 256;
+  static constexpr int KSLOT = 2 * DF * 4;            // [bias F | qmul F] floats
+  static constexpr int OFF_K = OFF_Z + ZB;
+  static constexpr int OFF_PG = OFF_K + 2 * KSLOT;    // pooled statistics, 2g doubles
+  static constexpr int OFF_C = OFF_PG + 2 * DG * 8;   // projected biases, F floats
+  static constexpr int TOWER_END = OFF_C + DF * 4;
+  static constexpr int OFF_X = BUF;                   // heads' bf16 input (int8: codes; bf16: lo part)
+  static constexpr int X_END = OFF_X + 64 * RBX;
+  static constexpr int OFF_S = 0;                     // query-key logits [64][64] f32
+  static constexpr int OFF_U = 64 * 64 * 4;           // value features [V][64] f32
+  static constexpr int OFF_O = OFF_U + 32 * 64 * 4;   // promotion offsets [8][4] f32
+  static constexpr int HEAD_END = OFF_O + 32 * 4;
+  static constexpr int SMEM = cmax(cmax(TOWER_END, X_END), HEAD_END);
+  static_assert(OFF_T >= 64 * 128, "stem input fits in the T buffer");
+  static constexpr int CPT = DF / T::KS;              // K steps per tap
+  static constexpr int S = 9 * CPT;                   // K steps per layer
+  static constexpr int NBUF = QUANT ? 5 : 3;          // weight ring (steps), loaded NBUF-1 ahead
+  static_assert((2 * S) % NBUF == 0, "every block's first conv starts at ring slot 0");
+  static constexpr int STEP_BYTES = DNMB * 64 * T::FB;
+  static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
+};
+
+template <int MK>
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 64), amdgpu_waves_per_eu(1, 1))) void
+az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal,
+              float* __restrict__ policy, float* __restrict__ value, float* __restrict__ wdl) {
+  using C = DepCfg<MK>;
+  using T = typename C::T;
+  using frag_t = typename T::frag;
+  using acc_t = typename T::acc;
+  using R = Rot<C::RB>;
+  constexpr bool QUANT = C::QUANT;
+  constexpr int RB = C::RB, OFF_H = C::OFF_H, OFF_T = C::OFF_T, OFF_Z = C::OFF_Z;
+
+  __shared__ __attribute__((aligned(16))) uint8_t smem[C::SMEM];
+
+  const int lane = threadIdx.x;
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int b = blockIdx.x;
+  const int Cin = p.in_planes;
+  const float cap = p.act_cap;
+
+  // fp32 residual stream of the board (bf16 networks): [block][half][16]
+  float res[QUANT ? 1 : DNMB][QUANT ? 1 : 2][16];
+
+  // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
+  for (int i = lane; i < C::ZB / 16; i += 64)
+    *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
+  for (int i = lane; i < DF; i += 64) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
+  {
+    // item k = planes 8k..8k+7: lane = square, eight coalesced loads, one 16-byte store
+    float pv[DCP / 8][8];
+#pragma unroll
+    for (int k = 0; k < DCP / 8; ++k)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int c = 8 * k + t;
+        const bool ok = c < Cin;
+        const float x = planes[((size_t)b * Cin + (ok ? c : 0)) * 64 + lane];
+        pv[k][t] = ok ? x : 0.0f;
+      }
+#pragma unroll
+    for (int k = 0; k < DCP / 8; ++k)
+      *reinterpret_cast<uint4*>(smem + OFF_T + lane * 128 + ((k ^ swz128(lane)) << 4)) =
+          make_uint4(pack_bf16x2(pv[k][0], pv[k][1]), pack_bf16x2(pv[k][2], pv[k][3]),
+                     pack_bf16x2(pv[k][4], pv[k][5]), pack_bf16x2(pv[k][6], pv[k][7]));
+  }
+
+  // tower weight ring: K step i of the stream lives in A[i % NBUF]
+  constexpr int NBUF = C::NBUF;
+  const uint8_t* tw = static_cast<const uint8_t*>(p.tower_w) + (size_t)lane * T::FB;
+  frag_t A[NBUF][DNMB];
+  auto load_step = [&](frag_t(&dst)[DNMB], const uint8_t* src) {
+#pragma unroll
+    for (int m = 0; m < DNMB; ++m) dst[m] = g_frag<MK>(src + m * 64 * T::FB);
+  };
+  static_for<0, NBUF - 1>([&](auto i_c) {
+    constexpr int i = decltype(i_c)::value;
+    load_step(A[i], tw + (size_t)i * C::STEP_BYTES);
+  });
+  // per-layer epilogue constants [bias F | qmul F] of conv index k (0 = stem) into slot
+  auto stage_consts = [&](int slot, int k) {
+    float* dst = reinterpret_cast<float*>(smem + C::OFF_K + slot * C::KSLOT);
+    for (int i = lane; i < DF / 4; i += 64) {
+      reinterpret_cast<float4*>(dst)[i] = *reinterpret_cast<const float4*>(p.bias + (size_t)k * DF + 4 * i);
+      if (QUANT) reinterpret_cast<float4*>(dst + DF)[i] = *reinterpret_cast<const float4*>(p.qmul + (size_t)k * DF + 4 * i);
+    }
+  };
+  stage_consts(0, 1);
+  __syncthreads();
+
+  // ---- stem: bf16 3x3 conv over 64 (padded) input channels, K = 576
+  {
+    constexpr int SSTEP = DNMB * 64 * 16;  // bytes per K step of the stem stream
+    const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)lane * 16;
+    f32x16 sacc[DNMB][2];
+    bf16x8 a[2][DNMB];  // A fragments of K step st in a[st & 1], loaded one step ahead
+    auto load_step_s = [&](bf16x8(&dst)[DNMB], int st) {
+#pragma unroll
+      for (int m = 0; m < DNMB; ++m) dst[m] = g_frag<MK_BF16>(sw8 + st * SSTEP + m * 64 * 16);
+    };
+    load_step_s(a[0], 0);
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) {
+      const int dy = tap / 3 - 1, dx = tap % 3 - 1;
+      int row[2], sw[2];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int j = n * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
+        const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
+        const int src = r * 8 + c;
+        row[n] = ok ? OFF_T + src * 128 : OFF_Z + ((src * 128) & 255);
+        sw[n] = swz128(src);
+      }
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int st = tap * 4 + s;
+        if (st + 1 < 36) load_step_s(a[(st + 1) & 1], st + 1);
+        bf16x8 bfr[2];
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+          bfr[n] = *reinterpret_cast<const bf16x8*>(smem + row[n] + (((2 * s + lhi) ^ sw[n]) << 4));
+#pragma unroll
+        for (int m = 0; m < DNMB; ++m)
+#pragma unroll
+          for (int n = 0; n < 2; ++n)
+            sacc[m][n] = mma_bf16(a[st & 1][m], bfr[n], st == 0 ? f32x16{} : sacc[m][n]);
+      }
+    }
+    // epilogue: bias, activation (codes for int8), store in the tower format at OFF_H
+#pragma unroll
+    for (int m = 0; m < DNMB; ++m)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ch0 = m * 32 + 8 * q + 4 * lhi;
+        const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
+        float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
+        if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+          const int j = n * 32 + l32;
+          const f32x16& v = sacc[m][n];
+          if constexpr (!QUANT) {
+            const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
+            const float y2 = act_fn(v[4 * q + 2] + bb.z, cap), y3 = act_fn(v[4 * q + 3] + bb.w, cap);
+            res[m][n][4 * q + 0] = y0;
+            res[m][n][4 * q + 1] = y1;
+            res[m][n][4 * q + 2] = y2;
+            res[m][n][4 * q + 3] = y3;
+            *reinterpret_cast<uint2*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi) =
+                make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+          } else {
+            const float hi = p.qhi[0];
+            const float z0 = med3(__builtin_fmaf(v[4 * q + 0], mm.x, bb.x), 0.0f, hi);
+            const float z1 = med3(__builtin_fmaf(v[4 * q + 1], mm.y, bb.y), 0.0f, hi);
+            const float z2 = med3(__builtin_fmaf(v[4 * q + 2], mm.z, bb.z), 0.0f, hi);
+            const float z3 = med3(__builtin_fmaf(v[4 * q + 3], mm.w, bb.w), 0.0f, hi);
+            *reinterpret_cast<uint32_t*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15)) =
+                pack_codes<MK>(z0, z1, z2, z3);
+          }
+        }
+      }
+  }
+  __syncthreads();
+
+  // ---- residual tower
+  {
+    constexpr int CPT = C::CPT;
+    acc_t c[DNMB][2];
+    const int nconv = 2 * p.blocks;
+
+    const int l32_ = l32, lhi_ = lhi;
+    auto conv = [&](auto second_c, auto pool_c, auto lb_c, int n_conv) {
+      constexpr bool SECOND = decltype(second_c)::value;
+      constexpr bool POOL = decltype(pool_c)::value;   // first conv of a pooling block
+      constexpr int LB = decltype(lb_c)::value;        // ring slot of the layer's first step
+      // lane coordinates, opaque to the compiler per layer, so that the layer's
+      // many lane-dependent addresses are computed in the layer instead of being
+      // hoisted out of the block loop and held (or spilled) across it
+      int l32 = l32_, lhi = lhi_;
+      asm volatile("" : "+v"(l32), "+v"(lhi));
+      const uint8_t* wl = tw + (size_t)n_conv * C::LAYER_BYTES;
+      const bool has_next = n_conv + 1 < nconv;
+      const int in_off = SECOND ? OFF_T : OFF_H;
+      const int out_off = SECOND ? OFF_H : OFF_T;
+      const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
+      // B fragments of one K step: rows of the current tap, chunk of channel step cs
+      int row[2], sw[2], nrow[2], nsw[2];
+      auto rows_for = [&](int tap, int(&rr)[2], int(&ss)[2]) {
+        const int dy = tap / 3 - 1, dx = tap % 3 - 1;
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+          const int j = n * 32 + l32, r = (j >> 3) + dy, cc = (j & 7) + dx;
+          const bool ok = (unsigned)r < 8u && (unsigned)cc < 8u;
+          const int src = r * 8 + cc;
+          const int ra = in_off + src * RB, rz = OFF_Z + ((src * RB) & 255);
+          const int msk = -(int)ok;
+          rr[n] = (ra & msk) | (rz & ~msk);
+          ss[n] = R::sw(src);
+        }
+      };
+      auto load_b = [&](const int(&rr)[2], const int(&ss)[2], int cs, frag_t(&dst)[2]) {
+        const int lc = 2 * cs + lhi;
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+          dst[n] = *reinterpret_cast<const frag_t*>(smem + rr[n] + (R::pos(lc, ss[n]) << 4));
+      };
+      frag_t bc[2], bn[2];
+      rows_for(0, row, sw);
+      load_b(row, sw, 0, bc);
+
+      // one tap: CPT K steps; R0 = ring slot of its first step
+      auto tap_body = [&](auto r0_c, auto first_c, int tap) {
+        constexpr int R0 = decltype(r0_c)::value;
+        constexpr bool FIRST = decltype(first_c)::value;
+        rows_for(tap + 1, nrow, nsw);
+        static_for<0, CPT>([&](auto cs_c) {
+          constexpr int cs = decltype(cs_c)::value;
+          constexpr int cur = (R0 + cs) % NBUF;
+          {
+            // step tap*CPT + cs + NBUF-1 of this layer (of the next layer past its end;
+            // past the network's last layer this layer is re-read and never used)
+            const int gi = tap * CPT + cs + NBUF - 1;
+            const uint8_t* nxt = wl + (size_t)gi * C::STEP_BYTES;
+            nxt = (has_next || gi < C::S) ? nxt : wl;
+            load_step(A[(cur + NBUF - 1) % NBUF], nxt);
+          }
+          if constexpr (cs + 1 < CPT) load_b(row, sw, cs + 1, bn);
+          else load_b(nrow, nsw, 0, bn);
+#pragma unroll
+          for (int m = 0; m < DNMB; ++m)
+#pragma unroll
+            for (int n = 0; n < 2; ++n)
+              c[m][n] = T::mma(A[cur][m], bc[n], (FIRST && cs == 0) ? acc_t{} : c[m][n]);
+#pragma unroll
+          for (int n = 0; n < 2; ++n) bc[n] = bn[n];
+          // each MFMA followed by one of the next step's LDS reads, then by one of
+          // the prefetched step's weight loads
+          static_for<0, DNMB * 2>([&](auto i_c) {
+            constexpr int i = decltype(i_c)::value;
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if constexpr (i < 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if constexpr (i < DNMB) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          });
+        });
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+          row[n] = nrow[n];
+          sw[n] = nsw[n];
+        }
+      };
+      constexpr int U = NBUF / gcd_c(CPT, NBUF), NIT = 8 / U, REM = 8 % U;
+      tap_body(std::integral_constant<int, LB>{}, std::true_type{}, 0);
+#pragma nounroll
+      for (int it = 0; it < NIT; ++it) {
+        static_for<0, U>([&](auto u_c) {
+          constexpr int u = decltype(u_c)::value;
+          tap_body(std::integral_constant<int, (LB + (1 + u) * CPT) % NBUF>{}, std::false_type{}, 1 + it * U + u);
+        });
+      }
+      static_for<0, REM>([&](auto u_c) {
+        constexpr int u = decltype(u_c)::value, t = 1 + NIT * U + u;
+        tap_body(std::integral_constant<int, (LB + t * CPT) % NBUF>{}, std::false_type{}, t);
+      });
+
+      // global pooling: pooled channels' board mean and maximum, projection to
+      // the regular channels' biases (LDS OFF_C)
+      float cinv = 1.0f;
+      if constexpr (POOL) {
+        cinv = p.pool_cinv[n_conv];
+        double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
+        static_for<0, DNMB * 4>([&](auto k_c) {
+          constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4;
+          if constexpr (32 * m + 8 * q >= DFR) {
+            const int ch0 = 32 * m + 8 * q + 4 * lhi;
+            const float4 mm = *reinterpret_cast<const float4*>(p.pool_m + (size_t)n_conv * DF + ch0);
+            const float4 bb = *reinterpret_cast<const float4*>(p.pool_b + (size_t)n_conv * DF + ch0);
+            const float mv[4] = {mm.x, mm.y, mm.z, mm.w}, bv[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float p0 = med3(__builtin_fmaf((float)c[m][0][4 * q + r], mv[r], bv[r]), 0.0f, cap);
+              const float p1 = med3(__builtin_fmaf((float)c[m][1][4 * q + r], mv[r], bv[r]), 0.0f, cap);
+              double s = (double)p0 + (double)p1;
+              float mx = fmaxf(p0, p1);
+#pragma unroll
+              for (int o = 1; o < 32; o <<= 1) {
+                s += shfl_xor_d(s, o);
+                mx = fmaxf(mx, __shfl_xor(mx, o));
+              }
+              if (l32 == 0) {
+                const int pc = ch0 + r - DFR;
+                pg[pc] = s * (1.0 / 64.0);
+                pg[DG + pc] = (double)mx;
+              }
+            }
+          }
+        });
+        wave_lds_sync();
+        // lane L: outputs L and L + 64 (those below Fr)
+        const double* wt = p.pool_wt + (size_t)(n_conv / 2 / p.pool_every) * (2 * DG * AZ_DEP_POOL_OPAD);
+        double c0 = 0.0, c1 = 0.0;
+#pragma unroll 8
+        for (int i = 0; i < 2 * DG; ++i) {
+          const double gi = pg[i];
+          c0 = __builtin_fma(wt[(size_t)i * AZ_DEP_POOL_OPAD + lane], gi, c0);
+          c1 = __builtin_fma(wt[(size_t)i * AZ_DEP_POOL_OPAD + 64 + lane], gi, c1);
+        }
+        float* cb = reinterpret_cast<float*>(smem + C::OFF_C);
+        cb[lane] = (float)c0;
+        if (lane + 64 < DFR) cb[lane + 64] = (float)c1;
+        wave_lds_sync();
+      }
+
+      // epilogue: per run of 4 channels; LDS reads of constants (and residual
+      // codes) issued two runs ahead
+      float hi = 0.0f, rq = 0.0f;
+      if constexpr (QUANT) {
+        hi = p.qhi[n_conv + 1];
+        rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
+      }
+      constexpr int NRUN = DNMB * 4, EP_AHEAD = QUANT ? 2 : 0, EP_RING = EP_AHEAD + 1;
+      constexpr bool RCODE = QUANT && SECOND;
+      float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
+      uint32_t rcode[RCODE ? EP_RING : 1][2];
+      auto ep_addr = [&](int m, int q, int n) {
+        const int j = n * 32 + l32;
+        const int ch0 = m * 32 + 8 * q + 4 * lhi;
+        const int rowo = out_off + j * RB;
+        if constexpr (QUANT) return rowo + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15);
+        else return rowo + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi;
+      };
+      auto ep_load = [&](auto k_c) {
+        constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
+        const int ch0 = m * 32 + 8 * q + 4 * lhi;
+        kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
+        if constexpr (QUANT) km[slot] = *reinterpret_cast<const float4*>(kslot + DF + ch0);
+        if constexpr (POOL) kc[slot] = *reinterpret_cast<const float4*>(smem + C::OFF_C + ch0 * 4);
+        if constexpr (RCODE) {
+#pragma unroll
+          for (int n = 0; n < 2; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
+        }
+      };
+      static_for<0, EP_AHEAD>([&](auto k_c) { ep_load(k_c); });
+      static_for<0, NRUN>([&](auto k_c) {
+        constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
+        if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
+        const float4 bb = kb[slot];
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+          const int addr = ep_addr(m, q, n);
+          const acc_t& v = c[m][n];
+          if constexpr (!QUANT) {
+            float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
+            float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
+            if constexpr (POOL) {
+              const float4 cc = kc[slot];
+              y0 += cc.x;
+              y1 += cc.y;
+              y2 += cc.z;
+              y3 += cc.w;
+            }
+            if constexpr (SECOND) {
+              y0 = act_fn(y0 + res[m][n][4 * q + 0], cap);
+              y1 = act_fn(y1 + res[m][n][4 * q + 1], cap);
+              y2 = act_fn(y2 + res[m][n][4 * q + 2], cap);
+              y3 = act_fn(y3 + res[m][n][4 * q + 3], cap);
+              res[m][n][4 * q + 0] = y0;
+              res[m][n][4 * q + 1] = y1;
+              res[m][n][4 * q + 2] = y2;
+              res[m][n][4 * q + 3] = y3;
+            } else {
+              y0 = act_fn(y0, cap);
+              y1 = act_fn(y1, cap);
+              y2 = act_fn(y2, cap);
+              y3 = act_fn(y3, cap);
+            }
+            *reinterpret_cast<uint2*>(smem + addr) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+          } else {
+            const float4 mm = km[slot];
+            float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
+            float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
+            float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
+            float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
+            if constexpr (POOL) {
+              const float4 cc = kc[slot];
+              z0 = __builtin_fmaf(cc.x, cinv, z0);
+              z1 = __builtin_fmaf(cc.y, cinv, z1);
+              z2 = __builtin_fmaf(cc.z, cinv, z2);
+              z3 = __builtin_fmaf(cc.w, cinv, z3);
+            }
+            if constexpr (SECOND) {
+              const uint32_t r = rcode[slot][n];
+              z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
+              z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
+              z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
+              z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
+            }
+            *reinterpret_cast<uint32_t*>(smem + addr) =
+                pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi), med3(z3, 0.0f, hi));
+          }
+        }
+      });
+      if (has_next) stage_consts((n_conv + 1) & 1, n_conv + 2);
+      __syncthreads();
+    };
+
+    for (int blk = 0; blk < p.blocks; ++blk) {
+      const bool pool = p.pool_every > 0 && blk % p.pool_every == p.pool_every - 1;
+      if (pool) conv(std::false_type{}, std::true_type{}, std::integral_constant<int, 0>{}, 2 * blk);
+      else conv(std::false_type{}, std::false_type{}, std::integral_constant<int, 0>{}, 2 * blk);
+      conv(std::true_type{}, std::false_type{}, std::integral_constant<int, C::S % NBUF>{}, 2 * blk + 1);
+    }
+  }
+
+  // ---- heads input: bf16 rows [square][F] at OFF_X (int8: the final codes'
+  // values, exact; bf16: the low part h - bf16(h) of the fp32 residual, H
+  // holding bf16(h))
+  using RX = Rot<C::RBX>;
+  if constexpr (QUANT) {
+    for (int idx = lane; idx < 64 * (DF / 8); idx += 64) {
+      const int k = idx % (DF / 8), sq = idx / (DF / 8);
+      const uint2 v = *reinterpret_cast<const uint2*>(smem + OFF_H + sq * RB + (R::pos(k >> 1, R::sw(sq)) << 4) + (k & 1) * 8);
+      const uint4 o = make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
+                                 pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
+                                 pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
+                                 pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y)));
+      *reinterpret_cast<uint4*>(smem + C::OFF_X + sq * C::RBX + (RX::pos(k, RX::sw(sq)) << 4)) = o;
+    }
+  } else {
+#pragma unroll
+    for (int m = 0; m < DNMB; ++m)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ch0 = m * 32 + 8 * q + 4 * lhi;
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+          const int j = n * 32 + l32;
+          float lo[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) lo[r] = res[m][n][4 * q + r] - bf16_round(res[m][n][4 * q + r]);
+          *reinterpret_cast<uint2*>(smem + C::OFF_X + j * C::RBX + (RX::pos(ch0 >> 3, RX::sw(j)) << 4) + 8 * lhi) =
+              make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+        }
+      }
+  }
+  __syncthreads();
+
+  // ---- embedding: E[row][sq] = sum_f Wemb[row][f] h[f][sq], rows = tokens then value channels
+  f32x16 tok[DTB][2];   // token rows (accumulators, then values)
+  f32x16 uacc[2];       // value rows 128..159
+  {
+    const uint8_t* ew = static_cast<const uint8_t*>(p.emb_w) + (size_t)lane * 16;
+#pragma unroll
+    for (int s = 0; s < DF / 16; ++s) {
+      bf16x8 aw[DEMB];
+#pragma unroll
+      for (int m = 0; m < DEMB; ++m) aw[m] = g_frag<MK_BF16>(ew + (s * DEMB + m) * 64 * 16);
+      bf16x8 bx[2], bh[2];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int j = n * 32 + l32;
+        bx[n] = *reinterpret_cast<const bf16x8*>(smem + C::OFF_X + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+        if constexpr (!QUANT)
+          bh[n] = *reinterpret_cast<const bf16x8*>(smem + OFF_H + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+      }
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+#pragma unroll
+        for (int m = 0; m < DTB; ++m) {
+          tok[m][n] = mma_bf16(aw[m], bx[n], s == 0 ? f32x16{} : tok[m][n]);
+          if constexpr (!QUANT) tok[m][n] = mma_bf16(aw[m], bh[n], tok[m][n]);
+        }
+        uacc[n] = mma_bf16(aw[DTB], bx[n], s == 0 ? f32x16{} : uacc[n]);
+        if constexpr (!QUANT) uacc[n] = mma_bf16(aw[DTB], bh[n], uacc[n]);
+      }
+    }
+  }
+  __syncthreads();  // H and X are dead from here on
+
+  // token values relu(acc * scale + bias); value features u[c][sq] to LDS
+  {
+#pragma unroll
+    for (int m = 0; m < DTB; ++m)
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int r0 = 32 * m + 8 * jq + 4 * lhi;
+        const float4 sc = *reinterpret_cast<const float4*>(p.emb_sc + r0);
+        const float4 bc = *reinterpret_cast<const float4*>(p.emb_bc + r0);
+        const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tok[m][n][4 * jq + r] = fmaxf(__builtin_fmaf(tok[m][n][4 * jq + r], sv[r], bv[r]), 0.0f);
+      }
+    float* U = reinterpret_cast<float*>(smem + C::OFF_U);
+    const int V = p.value_channels;
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      const int r0 = DD + 8 * jq + 4 * lhi;
+      const float4 sc = *reinterpret_cast<const float4*>(p.emb_sc + r0);
+      const float4 bc = *reinterpret_cast<const float4*>(p.emb_bc + r0);
+      const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ch = 8 * jq + 4 * lhi + r;
+        if (ch < V) {
+#pragma unroll
+          for (int n = 0; n < 2; ++n) {
+            float u = __builtin_fmaf(uacc[n][4 * jq + r], sv[r], bv[r]);
+            if (p.value_conv_relu) u = fmaxf(u, 0.0f);
+            U[ch * 64 + n * 32 + l32] = u;
+          }
+        }
+      }
+    }
+  }
+
+  // Operand fragments from accumulators: K step s of a 128-row accumulator
+  // set X[4][2] (rows = the product's K dimension) for column block n holds
+  // positions 8s .. 8s+7 of the lane's 64 accumulator values.
+  auto frags_of = [&](const f32x16(&X)[DTB][2], int n, int s, bf16x8& hi, bf16x8& lo) {
+    float x[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) x[t] = X[(8 * s + t) / 16][n][(8 * s + t) % 16];
+    split8(x, hi, lo);
+  };
+  // Q^T = Wq tok^T + bq and K^T = Wk tok^T + bk in one pass over the token
+  // fragments (split operands); rows of Q^T and K^T in the token accumulators'
+  // register order, so the token values die as the pass ends
+  f32x16 Qa[DTB][2], Ka[DTB][2];
+  {
+    const uint8_t* qp = static_cast<const uint8_t*>(p.q_w) + (size_t)lane * 16;
+    const uint8_t* kp = static_cast<const uint8_t*>(p.k_w) + (size_t)lane * 16;
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) {
+      bf16x8 aq[DTB], ak[DTB];
+#pragma unroll
+      for (int m = 0; m < DTB; ++m) {
+        aq[m] = g_frag<MK_BF16>(qp + (s * DTB + m) * 64 * 16);
+        ak[m] = g_frag<MK_BF16>(kp + (s * DTB + m) * 64 * 16);
+      }
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        bf16x8 xh, xl;
+        frags_of(tok, n, s, xh, xl);
+#pragma unroll
+        for (int m = 0; m < DTB; ++m) {
+          Qa[m][n] = mma_bf16(aq[m], xh, s == 0 ? f32x16{} : Qa[m][n]);
+          Qa[m][n] = mma_bf16(aq[m], xl, Qa[m][n]);
+          Ka[m][n] = mma_bf16(ak[m], xh, s == 0 ? f32x16{} : Ka[m][n]);
+          Ka[m][n] = mma_bf16(ak[m], xl, Ka[m][n]);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < DTB; ++m)
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int r0 = 32 * m + 8 * jq + 4 * lhi;
+        const float4 bq = *reinterpret_cast<const float4*>(p.q_b + r0);
+        const float4 bk = *reinterpret_cast<const float4*>(p.k_b + r0);
+        const float qv[4] = {bq.x, bq.y, bq.z, bq.w}, kv[4] = {bk.x, bk.y, bk.z, bk.w};
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            Qa[m][n][4 * jq + r] += qv[r];
+            Ka[m][n][4 * jq + r] += kv[r];
+          }
+      }
+  }
+
+  // S[f][t] = sum_d Q[f][d] K[t][d] (hi*hi + hi*lo + lo*hi) and the promotion
+  // offsets O^T[k][t] = sum_d Wp[k][d] K[t][d] for the last row's destinations
+  f32x16 Sa[2][2], Oa;
+  {
+    const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) {
+      bf16x8 qh[2], ql[2], kh[2], kl[2];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        frags_of(Qa, n, s, qh[n], ql[n]);
+        frags_of(Ka, n, s, kh[n], kl[n]);
+      }
+#pragma unroll
+      for (int mf = 0; mf < 2; ++mf)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          Sa[mf][nt] = mma_bf16(qh[mf], kh[nt], s == 0 ? f32x16{} : Sa[mf][nt]);
+          Sa[mf][nt] = mma_bf16(qh[mf], kl[nt], Sa[mf][nt]);
+          Sa[mf][nt] = mma_bf16(ql[mf], kh[nt], Sa[mf][nt]);
+        }
+      const bf16x8 aw = g_frag<MK_BF16>(pw + s * 64 * 16);
+      Oa = mma_bf16(aw, kh[1], s == 0 ? f32x16{} : Oa);
+      Oa = mma_bf16(aw, kl[1], Oa);
+    }
+  }
+  // logits pre-scaled by log2(e) for the exp2 softmax
+  {
+    const float log2e = 1.4426950408889634f;
+    const float ss = log2e / sqrtf((float)DD);
+    float* S = reinterpret_cast<float*>(smem + C::OFF_S);
+#pragma unroll
+    for (int mf = 0; mf < 2; ++mf)
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int f = 32 * mf + 8 * (v / 4) + 4 * lhi + v % 4, t = 32 * nt + l32;
+          S[f * 64 + t] = Sa[mf][nt][v] * ss;
+        }
+    float* O = reinterpret_cast<float*>(smem + C::OFF_O);
+    if (lhi == 0 && l32 >= 24) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) O[(l32 - 24) * 4 + k] = Oa[k] * log2e;
+    }
+  }
+  wave_lds_sync();
+
+  // ---- legal-action softmax: lane owns the runs of 4 actions at 256 i + 4 lane
+  {
+    constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
+    const float* S = reinterpret_cast<const float*>(smem + C::OFF_S);
+    const float* O = reinterpret_cast<const float*>(smem + C::OFF_O);
+    const uint8_t* lg = legal + (size_t)b * NA;
+    float e[NIT][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      const bool in = a0 < NA;  // NA is a multiple of 4
+      const uint4 tb = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
+      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
+      const uint32_t mk = in ? mk0 : 0u;
+      const uint32_t te[4] = {tb.x, tb.y, tb.z, tb.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t x = te[r], pr = x >> 12;
+        const float z = S[x & 4095u] + (pr ? O[pr - 1] : 0.0f);
+        const bool ok = in && ((mk >> (8 * r)) & 0xffu);
+        e[i][r] = ok ? z : -INFINITY;
+        mx = fmaxf(mx, e[i][r]);
+      }
+    }
+    mx = wave_max(mx);
+    const float msub = mx == -INFINITY ? 0.0f : mx;
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        e[i][r] = __builtin_amdgcn_exp2f(e[i][r] - msub);  // exp2(-inf) = 0
+        sum += e[i][r];
+      }
+    sum = wave_sum(sum);
+    const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
+    float* pol = policy + (size_t)b * NA;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      if (a0 < NA)
+        *reinterpret_cast<float4*>(pol + a0) = make_float4(e[i][0] * inv, e[i][1] * inv, e[i][2] * inv, e[i][3] * inv);
+    }
+  }
+
+  // ---- WDL head: y = relu(W1 u + b1), z = W2 y + b2, softmax, value = W - L
+  {
+    const float* U = reinterpret_cast<const float*>(smem + C::OFF_U);
+    const int H = p.value_hidden, NU = p.value_channels * 64;
+    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
+    for (int k0 = 0; k0 < H; k0 += 64) {
+      const int k = k0 + lane;
+      const bool ok = k < H;
+      const int kk = ok ? k : 0;
+      float y = p.wdl_fc1_b[kk];
+      for (int i = 0; i < NU; ++i) y = __builtin_fmaf(p.wdl_fc1_t[(size_t)i * H + kk], U[i], y);
+      y = ok ? fmaxf(y, 0.0f) : 0.0f;
+      z0 = __builtin_fmaf(p.wdl_fc2_w[kk], y, z0);
+      z1 = __builtin_fmaf(p.wdl_fc2_w[H + kk], y, z1);
+      z2 = __builtin_fmaf(p.wdl_fc2_w[2 * H + kk], y, z2);
+    }
+    z0 = wave_sum(z0) + p.wdl_fc2_b[0];
+    z1 = wave_sum(z1) + p.wdl_fc2_b[1];
+    z2 = wave_sum(z2) + p.wdl_fc2_b[2];
+    const float m = fmaxf(z0, fmaxf(z1, z2));
+    const float e0 = expf(z0 - m), e1 = expf(z1 - m), e2 = expf(z2 - m);
+    const float is = 1.0f / (e0 + e1 + e2);
+    if (lane == 0) {
+      const float pw = e0 * is, pd = e1 * is, pl = e2 * is;
+      value[b] = pw - pl;
+      if (wdl) {
+        wdl[3 * (size_t)b + 0] = pw;
+        wdl[3 * (size_t)b + 1] = pd;
+        wdl[3 * (size_t)b + 2] = pl;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t az_launch_deployed(int dtype, const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
+                              float* policy, float* value, float* wdl, hipStream_t s) {
+  (void)hipGetLastError();
+  if (n.filters != DF || B <= 0) return hipErrorInvalidValue;
+  if (dtype == AZ_INT8)
+    hipLaunchKernelGGL(az_dep_kernel<MK_I8>, dim3(B), dim3(64), 0, s, n, planes, legal, policy, value, wdl);
+  else if (dtype == AZ_BF16)
+    hipLaunchKernelGGL(az_dep_kernel<MK_BF16>, dim3(B), dim3(64), 0, s, n, planes, legal, policy, value, wdl);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}

@@ -102,9 +102,18 @@ __global__ __launch_bounds__(64 * COMPACT_ROWS_PER_BLOCK) void az_compact_policy
   uint4 m[COMPACT_MAX_PASSES];
 #pragma unroll
   for (int i = 0; i < COMPACT_MAX_PASSES; ++i) {
+    // NM is a multiple of 4 (P*64 cells, or the 1,880 from-to actions), so each
+    // 4-byte word of a lane's 16 bytes is either in the row or past its end;
+    // words past the end read as zero (not legal)
     const int c = i * COMPACT_PASS + 16 * lane;
-    // NM is a multiple of 64, so a lane's 16 bytes are all in the row or all past it
-    m[i] = c < NM ? *reinterpret_cast<const uint4*>(lg + c) : make_uint4(0u, 0u, 0u, 0u);
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cq = c + 4 * q;
+      const uint32_t v = *reinterpret_cast<const uint32_t*>(lg + (cq < NM ? cq : 0));  // clamped, unconditional
+      w[q] = cq < NM ? v : 0u;
+    }
+    m[i] = make_uint4(w[0], w[1], w[2], w[3]);
   }
   int base = 0;
 #pragma unroll
@@ -260,9 +269,9 @@ int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t fl
   const az_layer_spec& sp = az_net_spec(net);
   if (max_batch < 1 || max_batch > sp.max_batch)
     return az_fail(AZ_ERR_INVALID_ARG, "az_pipeline_create: max_batch must be 1..the handle's max_batch");
-  if (compact && max_legal > sp.policy_planes * AZ_SQUARES)
+  if (compact && max_legal > az_spec_moves(sp))
     return az_fail(AZ_ERR_INVALID_ARG, "az_pipeline_create: max_legal exceeds the number of policy cells");
-  if (sp.policy_planes * AZ_SQUARES > COMPACT_PASS * COMPACT_MAX_PASSES)
+  if (az_spec_moves(sp) > COMPACT_PASS * COMPACT_MAX_PASSES)
     return az_fail(AZ_ERR_UNSUPPORTED, "az_pipeline_create: policy rows too long");
   az_pipeline* p = new (std::nothrow) az_pipeline;
   if (!p) return az_fail(AZ_ERR_NOMEM, "az_pipeline_create: host allocation failed");
@@ -270,7 +279,7 @@ int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t fl
   p->device = az_net_device(net);
   p->max_batch = max_batch;
   p->in_planes = sp.in_planes;
-  p->n_moves = sp.policy_planes * AZ_SQUARES;
+  p->n_moves = az_spec_moves(sp);
   p->graphs = (flags & AZ_PIPE_GRAPHS) != 0;
   p->compact = compact;
   p->max_legal = max_legal;

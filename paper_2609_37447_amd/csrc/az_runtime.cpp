@@ -12,11 +12,18 @@
 // use the same k slots, so the pairing of A and B k values matches by
 // construction.  Order: stem (bf16), then the 2*blocks residual convs, then
 // the head: 96 rows (policy planes, value 1x1 conv row, zero rows), K = F.
+//
+// The deployed network (from-to policy, WDL value, global pooling) pads the
+// stem to 64 input channels, packs the second convolution of a pooling block
+// ([F][Fr][3][3]) with zero weights for input channels Fr..F-1, and packs its
+// heads as described in az_kernels_deployed.hip.
 #include "../../include/az.h"
 #include "az_internal.h"
 
 #include <math.h>
 #include <stdarg.h>
+#include <stddef.h>
+#include <stdlib.h>
 #include <stdio.h>
 #include <string.h>
 
@@ -54,59 +61,140 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(st, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool spec_well_formed(const az_layer_spec* s) {
-  return s && s->abi_version == AZ_ABI_VERSION && s->in_planes >= 1 && s->blocks >= 1 &&
-         s->filters >= 1 && s->policy_planes >= 1 && s->value_hidden >= 1 &&
-         (s->value_conv_relu == 0 || s->value_conv_relu == 1) && s->act_cap >= 0.0f &&
-         isfinite(s->act_cap) && s->max_batch >= 1;
+// Bytes of a version-1 spec: the fields before pool_every.
+constexpr size_t kSpecV1Bytes = offsetof(az_layer_spec, pool_every);
+
+// Copies a caller's spec into the current layout (version-1 callers pass the
+// first nine fields only: the move-plane network with the tanh value head).
+bool normalize_spec(const az_layer_spec* in, az_layer_spec* out) {
+  if (!in) return false;
+  if (in->abi_version == 1) {
+    memset(out, 0, sizeof *out);
+    memcpy(out, in, kSpecV1Bytes);
+    out->value_channels = 1;
+  } else if (in->abi_version == 2) {
+    *out = *in;
+  } else {
+    return false;
+  }
+  out->abi_version = AZ_ABI_VERSION;
+  return true;
 }
 
-int check_spec(const az_layer_spec* s, int dtype) {
+bool is_pool_block(const az_layer_spec& s, int j) {
+  return s.pool_every > 0 && j % s.pool_every == s.pool_every - 1;
+}
+
+bool is_deployed(const az_layer_spec& s) {
+  return s.policy_head == AZ_POLICY_FROMTO || s.value_head == AZ_VALUE_WDL || s.pool_every > 0;
+}
+
+bool spec_well_formed(const az_layer_spec& s) {
+  if (!(s.in_planes >= 1 && s.blocks >= 1 && s.filters >= 1 && s.value_hidden >= 1 &&
+        (s.value_conv_relu == 0 || s.value_conv_relu == 1) && s.act_cap >= 0.0f && isfinite(s.act_cap) &&
+        s.max_batch >= 1 && s.pool_every >= 0))
+    return false;
+  if (s.policy_head == AZ_POLICY_PLANES) {
+    if (s.policy_planes < 1 || s.token_dim != 0) return false;
+  } else if (s.policy_head == AZ_POLICY_FROMTO) {
+    if (s.policy_planes != 0 || s.token_dim < 1) return false;
+  } else {
+    return false;
+  }
+  if (s.value_head == AZ_VALUE_TANH) {
+    if (s.value_channels != 1) return false;
+  } else if (s.value_head == AZ_VALUE_WDL) {
+    if (s.value_channels < 1) return false;
+  } else {
+    return false;
+  }
+  return s.pool_every == 0 || s.filters % 4 == 0;
+}
+
+int check_spec(const az_layer_spec& s, int dtype) {
   if (!spec_well_formed(s)) return fail(AZ_ERR_INVALID_ARG, "malformed az_layer_spec");
   if (dtype < AZ_F32 || dtype > AZ_FP8_E4M3) return fail(AZ_ERR_INVALID_ARG, "unknown dtype %d", dtype);
-  if (s->in_planes > AZ_MAX_IN_PLANES) return fail(AZ_ERR_UNSUPPORTED, "in_planes %d > %d", s->in_planes, AZ_MAX_IN_PLANES);
-  if (s->blocks > 64) return fail(AZ_ERR_UNSUPPORTED, "blocks %d > 64", s->blocks);
-  if (s->policy_planes > AZ_MAX_POLICY) return fail(AZ_ERR_UNSUPPORTED, "policy_planes %d > %d", s->policy_planes, AZ_MAX_POLICY);
-  if (s->value_hidden > 512) return fail(AZ_ERR_UNSUPPORTED, "value_hidden %d > 512", s->value_hidden);
-  if (s->max_batch > (1 << 20)) return fail(AZ_ERR_UNSUPPORTED, "max_batch %d > 2^20", s->max_batch);
+  if (s.blocks > 64) return fail(AZ_ERR_UNSUPPORTED, "blocks %d > 64", s.blocks);
+  if (s.value_hidden > 512) return fail(AZ_ERR_UNSUPPORTED, "value_hidden %d > 512", s.value_hidden);
+  if (s.max_batch > (1 << 20)) return fail(AZ_ERR_UNSUPPORTED, "max_batch %d > 2^20", s.max_batch);
+  if (is_deployed(s)) {
+    if (s.policy_head != AZ_POLICY_FROMTO || s.value_head != AZ_VALUE_WDL)
+      return fail(AZ_ERR_UNSUPPORTED, "global pooling, the from-to policy and the WDL value head come together");
+    if (dtype != AZ_BF16 && dtype != AZ_INT8) return fail(AZ_ERR_UNSUPPORTED, "the deployed network runs in AZ_BF16 or AZ_INT8");
+    if (s.filters != 160) return fail(AZ_ERR_UNSUPPORTED, "the deployed network needs filters 160, got %d", s.filters);
+    if (s.token_dim != AZ_DEP_TOKEN) return fail(AZ_ERR_UNSUPPORTED, "token_dim %d != %d", s.token_dim, AZ_DEP_TOKEN);
+    if (s.value_channels > AZ_DEP_EMB_ROWS - AZ_DEP_TOKEN)
+      return fail(AZ_ERR_UNSUPPORTED, "value_channels %d > %d", s.value_channels, AZ_DEP_EMB_ROWS - AZ_DEP_TOKEN);
+    if (s.in_planes > AZ_DEP_MAX_IN_PLANES) return fail(AZ_ERR_UNSUPPORTED, "in_planes %d > %d", s.in_planes, AZ_DEP_MAX_IN_PLANES);
+    return AZ_OK;
+  }
+  if (s.in_planes > AZ_MAX_IN_PLANES) return fail(AZ_ERR_UNSUPPORTED, "in_planes %d > %d", s.in_planes, AZ_MAX_IN_PLANES);
+  if (s.policy_planes > AZ_MAX_POLICY) return fail(AZ_ERR_UNSUPPORTED, "policy_planes %d > %d", s.policy_planes, AZ_MAX_POLICY);
   if (dtype == AZ_F32) {
-    if (s->filters % 8 != 0 || s->filters > 256) return fail(AZ_ERR_UNSUPPORTED, "AZ_F32 needs filters a multiple of 8 up to 256, got %d", s->filters);
-  } else if (!az_mfma_supported(dtype, s->filters)) {
-    return fail(AZ_ERR_UNSUPPORTED, "dtype %d needs filters in {64, 128, 256}, got %d", dtype, s->filters);
+    if (s.filters % 8 != 0 || s.filters > 256) return fail(AZ_ERR_UNSUPPORTED, "AZ_F32 needs filters a multiple of 8 up to 256, got %d", s.filters);
+  } else if (!az_mfma_supported(dtype, s.filters)) {
+    return fail(AZ_ERR_UNSUPPORTED, "dtype %d needs filters in {64, 128, 256}, got %d", dtype, s.filters);
   }
   return AZ_OK;
 }
 
-size_t weight_count(const az_layer_spec* s) {
-  const size_t C = s->in_planes, F = s->filters, P = s->policy_planes, H = s->value_hidden;
-  return F * C * 9 + F + (size_t)s->blocks * 2 * (F * F * 9 + F) + P * F + P + F + 1 + H * 64 + H + H + 1;
+size_t weight_count(const az_layer_spec& s) {
+  const size_t C = s.in_planes, F = s.filters, P = s.policy_planes, H = s.value_hidden;
+  const size_t g = s.pool_every > 0 ? F / 4 : 0, Fr = F - g, D = s.token_dim, V = s.value_channels;
+  size_t n = F * C * 9 + F;
+  for (int j = 0; j < s.blocks; ++j)
+    n += F * F * 9 + F + (is_pool_block(s, j) ? Fr * 2 * g + F * Fr * 9 + F : F * F * 9 + F);
+  n += s.policy_head == AZ_POLICY_FROMTO ? D * F + D + 2 * (D * D + D) + 4 * D : P * F + P;
+  n += s.value_head == AZ_VALUE_WDL ? V * F + V + H * V * 64 + H + 3 * H + 3 : F + 1 + H * 64 + H + H + 1;
+  return n;
 }
 
 // Offsets of the arrays inside the canonical blob.
 struct BlobView {
   const float *stem_w, *stem_b, *pol_w, *pol_b, *val_w, *val_b, *fc1_w, *fc1_b, *fc2_w, *fc2_b;
   std::vector<const float*> w, b;  // residual conv n = 2j (first) and 2j+1 (second)
+  std::vector<const float*> pool;  // per block: Wg [Fr][2g] or NULL
+  // from-to head
+  const float *emb_w = nullptr, *emb_b = nullptr, *q_w = nullptr, *q_b = nullptr, *k_w = nullptr,
+              *k_b = nullptr, *p_w = nullptr;
 };
 
-BlobView view(const az_layer_spec* s, const float* blob) {
-  const size_t C = s->in_planes, F = s->filters, P = s->policy_planes, H = s->value_hidden;
+BlobView view(const az_layer_spec& s, const float* blob) {
+  const size_t C = s.in_planes, F = s.filters, P = s.policy_planes, H = s.value_hidden;
+  const size_t g = s.pool_every > 0 ? F / 4 : 0, Fr = F - g, D = s.token_dim, V = s.value_channels;
   BlobView v;
   const float* q = blob;
   v.stem_w = q; q += F * C * 9;
   v.stem_b = q; q += F;
-  for (int j = 0; j < s->blocks; ++j)
-    for (int k = 0; k < 2; ++k) {
-      v.w.push_back(q); q += F * F * 9;
-      v.b.push_back(q); q += F;
-    }
-  v.pol_w = q; q += P * F;
-  v.pol_b = q; q += P;
-  v.val_w = q; q += F;
-  v.val_b = q; q += 1;
-  v.fc1_w = q; q += H * 64;
+  for (int j = 0; j < s.blocks; ++j) {
+    const bool pool = is_pool_block(s, j);
+    v.w.push_back(q); q += F * F * 9;
+    v.b.push_back(q); q += F;
+    v.pool.push_back(pool ? q : nullptr);
+    if (pool) q += Fr * 2 * g;
+    v.w.push_back(q); q += F * (pool ? Fr : F) * 9;
+    v.b.push_back(q); q += F;
+  }
+  if (s.policy_head == AZ_POLICY_FROMTO) {
+    v.emb_w = q; q += D * F;
+    v.emb_b = q; q += D;
+    v.q_w = q; q += D * D;
+    v.q_b = q; q += D;
+    v.k_w = q; q += D * D;
+    v.k_b = q; q += D;
+    v.p_w = q; q += 4 * D;
+    v.pol_w = v.pol_b = nullptr;
+  } else {
+    v.pol_w = q; q += P * F;
+    v.pol_b = q; q += P;
+  }
+  const size_t VR = s.value_head == AZ_VALUE_WDL ? V : 1;
+  v.val_w = q; q += VR * F;
+  v.val_b = q; q += VR;
+  v.fc1_w = q; q += H * VR * 64;
   v.fc1_b = q; q += H;
-  v.fc2_w = q; q += H;
-  v.fc2_b = q; q += 1;
+  v.fc2_w = q; q += (s.value_head == AZ_VALUE_WDL ? 3 : 1) * H;
+  v.fc2_b = q; q += s.value_head == AZ_VALUE_WDL ? 3 : 1;
   return v;
 }
 
@@ -194,6 +282,63 @@ void pack_head(const BlobView& v, int F, int P, std::vector<uint8_t>& out) {
       }
 }
 
+// ---- deployed network -------------------------------------------------------
+//
+// bf16 A fragments of a row-major matrix M[rows][K] (rows padded with zeros to
+// nMB*32, K a multiple of 16): fragment (s, mb), lane l holds
+// M[mb*32 + l%32][kperm(s, l/32, t)], t = 0..7.  The plain order is
+// kperm = s*16 + 8*(l/32) + t.
+template <class KPerm>
+void pack_rows_bf16(const float* M, int rows, int K, int nMB, KPerm kperm, std::vector<uint8_t>& out) {
+  const int S = K / 16;
+  const size_t base = out.size();
+  out.resize(base + (size_t)S * nMB * 64 * 16);
+  uint8_t* o = out.data() + base;
+  for (int s = 0; s < S; ++s)
+    for (int mb = 0; mb < nMB; ++mb)
+      for (int l = 0; l < 64; ++l) {
+        const int row = mb * 32 + l % 32;
+        for (int t = 0; t < 8; ++t) {
+          const float w = row < rows ? M[(size_t)row * K + kperm(s, l / 32, t)] : 0.0f;
+          const uint16_t h = bf16_rne(w);
+          memcpy(o + ((size_t)(s * nMB + mb) * 64 + l) * 16 + 2 * t, &h, 2);
+        }
+      }
+}
+
+// Row index held at position p (0..63) of the accumulators of lane half lhi of
+// an output with 128 rows (four 32-row blocks): block p/16, register v = p%16,
+// row 32*(p/16) + 8*(v/4) + 4*lhi + v%4.  The token, query and key
+// accumulators feed the next products directly as operands: K step s, lane
+// half lhi, slot t carries position 8*s + t, so the weights that multiply them
+// are packed with their K dimension in this order.
+int acc_row(int s, int lhi, int t) {
+  const int p = 8 * s + t, v = p % 16;
+  return 32 * (p / 16) + 8 * (v / 4) + 4 * lhi + v % 4;
+}
+
+// Action table of the from-to policy: origin-destination pairs on a common
+// row, column or diagonal or a knight's jump apart, ascending (origin,
+// destination); then the promotions from row 6 to row 7 at most one column
+// over, pieces queen, rook, bishop, knight, ascending (origin, destination,
+// piece).  Entry: origin*64 + destination, plus (column*4 + piece + 1) << 12
+// for a promotion (its offset O[column][piece]).
+std::vector<uint32_t> fromto_actions() {
+  std::vector<uint32_t> a;
+  for (int f = 0; f < 64; ++f)
+    for (int t = 0; t < 64; ++t) {
+      if (t == f) continue;
+      const int dr = abs(t / 8 - f / 8), dc = abs(t % 8 - f % 8);
+      if (dr == 0 || dc == 0 || dr == dc || (dr == 1 && dc == 2) || (dr == 2 && dc == 1))
+        a.push_back((uint32_t)(f * 64 + t));
+    }
+  for (int fc = 0; fc < 8; ++fc)
+    for (int tc = fc > 0 ? fc - 1 : 0; tc <= (fc < 7 ? fc + 1 : 7); ++tc)
+      for (int k = 0; k < 4; ++k)
+        a.push_back((uint32_t)((48 + fc) * 64 + 56 + tc) | ((uint32_t)(tc * 4 + k + 1) << 12));
+  return a;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Measured on MI355X (20x128 and 24x256 networks): one board per workgroup wins
@@ -201,7 +346,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // workgroups per compute unit) wins for int8 / fp8 and the four-board large
 // tiling for bf16.
 int choose_tiling(const az_net* n, int B) {
-  if (n->dtype == AZ_F32) return 0;
+  if (n->dtype == AZ_F32 || is_deployed(n->spec)) return 0;
   if (n->tiling) return n->tiling;
   const int F = n->spec.filters;
   if (B < 512) return 2;
@@ -216,13 +361,17 @@ int choose_tiling(const az_net* n, int B) {
 int az_fail(int status, const char* detail) { return fail(status, "%s", detail); }
 
 const az_layer_spec& az_net_spec(const az_net* n) { return n->spec; }
+int az_spec_moves(const az_layer_spec& s) {
+  return s.policy_head == AZ_POLICY_FROMTO ? AZ_FROMTO_ACTIONS : s.policy_planes * AZ_SQUARES;
+}
 int az_net_device(const az_net* n) { return n->device; }
 
 extern "C" {
 
 size_t az_weight_count(const az_layer_spec* spec) {
-  if (!spec_well_formed(spec)) return 0;
-  return weight_count(spec);
+  az_layer_spec s;
+  if (!normalize_spec(spec, &s) || !spec_well_formed(s)) return 0;
+  return weight_count(s);
 }
 
 const char* az_status_string(int status) {
@@ -238,18 +387,20 @@ const char* az_status_string(int status) {
 
 const char* az_last_error(void) { return g_err.c_str(); }
 
-int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weights, int32_t dtype,
+int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_weights, int32_t dtype,
                 const float* w_scales, size_t n_w_scales, const float* act_scales,
                 size_t n_act_scales, az_net** out) {
   g_err.clear();
   if (!out || !weights) return fail(AZ_ERR_INVALID_ARG, "NULL weights or out pointer");
-  int st = check_spec(spec, dtype);
+  az_layer_spec s;
+  if (!normalize_spec(spec_in, &s)) return fail(AZ_ERR_INVALID_ARG, "malformed az_layer_spec");
+  int st = check_spec(s, dtype);
   if (st != AZ_OK) return st;
-  const az_layer_spec& s = *spec;
-  if (n_weights != weight_count(spec))
-    return fail(AZ_ERR_INVALID_ARG, "n_weights %zu, the spec needs %zu", n_weights, weight_count(spec));
+  if (n_weights != weight_count(s))
+    return fail(AZ_ERR_INVALID_ARG, "n_weights %zu, the spec needs %zu", n_weights, weight_count(s));
   const int F = s.filters, NB = s.blocks, P = s.policy_planes, H = s.value_hidden, Cin = s.in_planes;
   const bool quant = dtype == AZ_INT8 || dtype == AZ_FP8_E4M3;
+  const bool dep = is_deployed(s);
   if (quant) {
     if (!w_scales || n_w_scales != (size_t)2 * NB * F)
       return fail(AZ_ERR_INVALID_ARG, "need %d weight scales, got %zu", 2 * NB * F, n_w_scales);
@@ -263,35 +414,41 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
     return fail(AZ_ERR_INVALID_ARG, "scales are only taken for AZ_INT8 and AZ_FP8_E4M3");
   }
 
-  const BlobView v = view(spec, weights);
-  std::vector<uint8_t> stem, tower, head;
+  const BlobView v = view(s, weights);
+  const int g = s.pool_every > 0 ? F / 4 : 0, Fr = F - g, V = s.value_channels, D = s.token_dim;
+  std::vector<uint8_t> stem, tower, head, emb, qw, kw, pw;
   std::vector<float> bias, qmul, qres, qhi, head_b, fc2w, head_sc, head_bc, fc1t;
+  std::vector<float> emb_sc, emb_bc, pool_m, pool_b, pool_cinv, wfc1t;
+  std::vector<double> pool_wt;
+  std::vector<uint32_t> actions;
   const float hs = quant ? act_scales[2 * NB] : 1.0f;
   try {
     bias.resize((size_t)(1 + 2 * NB) * F);
-    head_b.assign(AZ_HEAD_ROWS, 0.0f);
-    fc2w.assign(v.fc2_w, v.fc2_w + H);
     memcpy(bias.data(), v.stem_b, F * sizeof(float));
     for (int n = 0; n < 2 * NB; ++n) memcpy(bias.data() + (size_t)(1 + n) * F, v.b[n], F * sizeof(float));
-    for (int i = 0; i < P; ++i) head_b[i] = v.pol_b[i];
-    head_b[P] = v.val_b[0];
-    // MFMA kernels: every head row r stores fma(acc, head_sc[r], head_bc[r]); policy
-    // rows come out pre-scaled by log2(e) for the exp2 softmax, the value row P
-    // unscaled, padding rows zero.  Products rounded once to float32.
-    const float log2e = 1.4426950408889634f;
-    head_sc.assign(AZ_HEAD_ROWS, 0.0f);
-    head_bc.assign(AZ_HEAD_ROWS, 0.0f);
-    for (int i = 0; i < P; ++i) {
-      head_sc[i] = hs * log2e;
-      head_bc[i] = v.pol_b[i] * log2e;
+    if (!dep) {
+      head_b.assign(AZ_HEAD_ROWS, 0.0f);
+      fc2w.assign(v.fc2_w, v.fc2_w + H);
+      for (int i = 0; i < P; ++i) head_b[i] = v.pol_b[i];
+      head_b[P] = v.val_b[0];
+      // MFMA kernels: every head row r stores fma(acc, head_sc[r], head_bc[r]); policy
+      // rows come out pre-scaled by log2(e) for the exp2 softmax, the value row P
+      // unscaled, padding rows zero.  Products rounded once to float32.
+      const float log2e = 1.4426950408889634f;
+      head_sc.assign(AZ_HEAD_ROWS, 0.0f);
+      head_bc.assign(AZ_HEAD_ROWS, 0.0f);
+      for (int i = 0; i < P; ++i) {
+        head_sc[i] = hs * log2e;
+        head_bc[i] = v.pol_b[i] * log2e;
+      }
+      head_sc[P] = hs;
+      head_bc[P] = v.val_b[0];
+      // fc1 for the MFMA kernels as [64/4][H][4]: lane k of a wave reads
+      // W1[k][4s .. 4s+3] at ((s * H + k) * 4), so a wave's float4 loads are contiguous.
+      fc1t.resize((size_t)H * 64);
+      for (int k = 0; k < H; ++k)
+        for (int c = 0; c < 64; ++c) fc1t[((size_t)(c / 4) * H + k) * 4 + (c % 4)] = v.fc1_w[(size_t)k * 64 + c];
     }
-    head_sc[P] = hs;
-    head_bc[P] = v.val_b[0];
-    // fc1 for the MFMA kernels as [64/4][H][4]: lane k of a wave reads
-    // W1[k][4s .. 4s+3] at ((s * H + k) * 4), so a wave's float4 loads are contiguous.
-    fc1t.resize((size_t)H * 64);
-    for (int k = 0; k < H; ++k)
-      for (int c = 0; c < 64; ++c) fc1t[((size_t)(c / 4) * H + k) * 4 + (c % 4)] = v.fc1_w[(size_t)k * 64 + c];
     if (dtype == AZ_F32) {
       // fp32 kernel: convs as [F/8][C][9][8] and heads as [ceil((P+1)/8)][F][8], so
       // that the eight output channels (rows) a thread accumulates at one (input
@@ -318,10 +475,14 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
             h[((size_t)rb * F + f) * 8 + j] = row < P ? v.pol_w[(size_t)row * F + f] : row == P ? v.val_w[f] : 0.0f;
           }
     } else {
-      pack_conv(v.stem_w, nullptr, F, Cin, 32, K_BF16, stem);
+      pack_conv(v.stem_w, nullptr, F, Cin, dep ? AZ_DEP_MAX_IN_PLANES : 32, K_BF16, stem);
       const Kind kind = dtype == AZ_BF16 ? K_BF16 : dtype == AZ_INT8 ? K_I8 : K_F8;
-      for (int n = 0; n < 2 * NB; ++n) pack_conv(v.w[n], quant ? w_scales + (size_t)n * F : nullptr, F, F, F, kind, tower);
-      pack_head(v, F, P, head);
+      for (int n = 0; n < 2 * NB; ++n) {
+        // the second convolution of a pooling block reads the Fr regular channels
+        const int cin = (n % 2 == 1 && is_pool_block(s, n / 2)) ? Fr : F;
+        pack_conv(v.w[n], quant ? w_scales + (size_t)n * F : nullptr, F, cin, F, kind, tower);
+      }
+      if (!dep) pack_head(v, F, P, head);
       if (quant) {
         // Requantising multiply-add constants; every product of two float32
         // values is rounded once to float32, in this order.
@@ -348,6 +509,50 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
           qhi[k] = c < qmax ? c : qmax;
         }
       }
+      if (dep) {
+        // global pooling: the pooled channels' pre-activation p = fma(acc, m, b)
+        // and the factor of the projected bias c in the regular channels' update
+        pool_m.assign((size_t)2 * NB * F, 1.0f);
+        pool_b.assign((size_t)2 * NB * F, 0.0f);
+        pool_cinv.assign((size_t)2 * NB, 1.0f);
+        for (int j = 0; j < NB; ++j) {
+          if (!is_pool_block(s, j)) continue;
+          const int n = 2 * j;
+          for (int f = 0; f < F; ++f) {
+            pool_b[(size_t)n * F + f] = v.b[n][f];
+            if (quant) pool_m[(size_t)n * F + f] = act_scales[n] * w_scales[(size_t)n * F + f];
+          }
+          if (quant) pool_cinv[n] = (float)(1.0 / (double)act_scales[n + 1]);
+          // Wg^T in fp64, outputs padded to AZ_DEP_POOL_OPAD
+          const size_t base = pool_wt.size();
+          pool_wt.resize(base + (size_t)2 * g * AZ_DEP_POOL_OPAD, 0.0);
+          for (int i = 0; i < 2 * g; ++i)
+            for (int o = 0; o < Fr; ++o) pool_wt[base + (size_t)i * AZ_DEP_POOL_OPAD + o] = v.pool[j][(size_t)o * 2 * g + i];
+        }
+        // embedding: D token rows (We) then V value rows (Wv), K = F, plain K order
+        std::vector<float> E((size_t)AZ_DEP_EMB_ROWS * F, 0.0f);
+        memcpy(E.data(), v.emb_w, (size_t)D * F * sizeof(float));
+        memcpy(E.data() + (size_t)D * F, v.val_w, (size_t)V * F * sizeof(float));
+        pack_rows_bf16(E.data(), D + V, F, AZ_DEP_EMB_ROWS / 32,
+                       [](int st, int lhi, int t) { return st * 16 + 8 * lhi + t; }, emb);
+        emb_sc.assign(AZ_DEP_EMB_ROWS, 0.0f);
+        emb_bc.assign(AZ_DEP_EMB_ROWS, 0.0f);
+        for (int r = 0; r < D + V; ++r) {
+          emb_sc[r] = hs;
+          emb_bc[r] = r < D ? v.emb_b[r] : v.val_b[r - D];
+        }
+        // query, key and promotion weights: K dimension in the accumulators' order
+        pack_rows_bf16(v.q_w, D, D, D / 32, acc_row, qw);
+        pack_rows_bf16(v.k_w, D, D, D / 32, acc_row, kw);
+        pack_rows_bf16(v.p_w, 4, D, 1, acc_row, pw);
+        // WDL: fc1 transposed to [V*64][H] so that lane k's loads are contiguous
+        wfc1t.resize((size_t)V * 64 * H);
+        for (int k = 0; k < H; ++k)
+          for (int i = 0; i < V * 64; ++i) wfc1t[(size_t)i * H + k] = v.fc1_w[(size_t)k * V * 64 + i];
+        actions = fromto_actions();
+        if (actions.size() != AZ_FROMTO_ACTIONS) return fail(AZ_ERR_DEVICE, "action table has %zu entries", actions.size());
+        actions.resize(AZ_DEP_ACTION_SLOTS, 0u);
+      }
     }
   } catch (const std::bad_alloc&) {
     return fail(AZ_ERR_NOMEM, "host allocation failed while packing weights");
@@ -355,14 +560,22 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
 
   // One device allocation, 256-byte aligned sections.
   struct Sec { const void* src; size_t bytes; size_t off; };
+  const size_t VH = dep ? (size_t)V * 64 * H : (size_t)H * 64;
   std::vector<Sec> secs = {
       {stem.data(), stem.size(), 0}, {tower.data(), tower.size(), 0}, {head.data(), head.size(), 0},
       {bias.data(), bias.size() * 4, 0}, {qmul.data(), qmul.size() * 4, 0},
       {qres.data(), qres.size() * 4, 0}, {qhi.data(), qhi.size() * 4, 0},
-      {head_b.data(), head_b.size() * 4, 0}, {v.fc1_w, (size_t)H * 64 * 4, 0},
-      {v.fc1_b, (size_t)H * 4, 0}, {fc2w.data(), fc2w.size() * 4, 0},
+      {head_b.data(), head_b.size() * 4, 0}, {dep ? nullptr : v.fc1_w, dep ? 0 : VH * 4, 0},
+      {v.fc1_b, (size_t)H * 4, 0}, {dep ? (const void*)v.fc2_w : fc2w.data(), (dep ? 3 : 1) * (size_t)H * 4, 0},
       {head_sc.data(), head_sc.size() * 4, 0}, {head_bc.data(), head_bc.size() * 4, 0},
-      {fc1t.data(), fc1t.size() * 4, 0}};
+      {fc1t.data(), fc1t.size() * 4, 0},
+      // deployed network
+      {emb.data(), emb.size(), 0}, {qw.data(), qw.size(), 0}, {kw.data(), kw.size(), 0},
+      {pw.data(), pw.size(), 0}, {emb_sc.data(), emb_sc.size() * 4, 0}, {emb_bc.data(), emb_bc.size() * 4, 0},
+      {dep ? v.q_b : nullptr, dep ? (size_t)D * 4 : 0, 0}, {dep ? v.k_b : nullptr, dep ? (size_t)D * 4 : 0, 0},
+      {pool_wt.data(), pool_wt.size() * 8, 0}, {pool_m.data(), pool_m.size() * 4, 0},
+      {pool_b.data(), pool_b.size() * 4, 0}, {pool_cinv.data(), pool_cinv.size() * 4, 0},
+      {actions.data(), actions.size() * 4, 0}, {wfc1t.data(), wfc1t.size() * 4, 0}};
   size_t total = 0;
   for (auto& sc : secs) { sc.off = total; total += align256(sc.bytes); }
 
@@ -380,6 +593,7 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   az_net* net = new (std::nothrow) az_net;
   if (!net) { (void)hipFree(dmem); return fail(AZ_ERR_NOMEM, "host allocation of the handle failed"); }
   auto at = [&](int i) { return secs[i].bytes ? static_cast<uint8_t*>(dmem) + secs[i].off : nullptr; };
+  auto atf = [&](int i) { return reinterpret_cast<const float*>(at(i)); };
   net->spec = s;
   net->dtype = dtype;
   net->device = dev;
@@ -387,6 +601,7 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   net->dmem = dmem;
   net->dbytes = total;
   AzDevNet& d = net->dn;
+  memset(&d, 0, sizeof d);
   d.in_planes = Cin;
   d.blocks = NB;
   d.filters = F;
@@ -398,38 +613,63 @@ int az_net_load(const az_layer_spec* spec, const float* weights, size_t n_weight
   d.stem_w = at(0);
   d.tower_w = at(1);
   d.head_w = at(2);
-  d.bias = reinterpret_cast<const float*>(at(3));
-  d.qmul = reinterpret_cast<const float*>(at(4));
-  d.qres = reinterpret_cast<const float*>(at(5));
-  d.qhi = reinterpret_cast<const float*>(at(6));
-  d.head_b = reinterpret_cast<const float*>(at(7));
-  d.fc1_w = reinterpret_cast<const float*>(at(8));
-  d.fc1_b = reinterpret_cast<const float*>(at(9));
-  d.fc2_w = reinterpret_cast<const float*>(at(10));
-  d.head_sc = reinterpret_cast<const float*>(at(11));
-  d.head_bc = reinterpret_cast<const float*>(at(12));
-  d.fc1_t = reinterpret_cast<const float*>(at(13));
-  d.fc2_b = v.fc2_b[0];
+  d.bias = atf(3);
+  d.qmul = atf(4);
+  d.qres = atf(5);
+  d.qhi = atf(6);
+  d.head_b = atf(7);
+  d.fc1_w = atf(8);
+  d.fc1_b = atf(9);
+  d.fc2_w = atf(10);
+  d.head_sc = atf(11);
+  d.head_bc = atf(12);
+  d.fc1_t = atf(13);
+  d.fc2_b = dep ? 0.0f : v.fc2_b[0];
+  if (dep) {
+    d.pool_every = s.pool_every;
+    d.value_channels = V;
+    d.emb_w = at(14);
+    d.q_w = at(15);
+    d.k_w = at(16);
+    d.p_w = at(17);
+    d.emb_sc = atf(18);
+    d.emb_bc = atf(19);
+    d.q_b = atf(20);
+    d.k_b = atf(21);
+    d.pool_wt = reinterpret_cast<const double*>(at(22));
+    d.pool_m = atf(23);
+    d.pool_b = atf(24);
+    d.pool_cinv = atf(25);
+    d.actions = reinterpret_cast<const uint32_t*>(at(26));
+    d.wdl_fc1_t = atf(27);
+    d.wdl_fc1_b = atf(9);
+    d.wdl_fc2_w = atf(10);
+    for (int i = 0; i < 3; ++i) d.wdl_fc2_b[i] = v.fc2_b[i];
+  }
   *out = net;
   return AZ_OK;
 }
 
-int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_t B, float* policy,
-                  float* value, void* stream) {
+int az_eval_batch_wdl(az_net* net, const float* planes, const uint8_t* legal, int32_t B, float* policy,
+                      float* value, float* wdl, void* stream) {
   if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
   if (B < 0) return fail(AZ_ERR_INVALID_ARG, "B = %d < 0", B);
+  const bool dep = is_deployed(net->spec);
+  if (wdl && !dep) return fail(AZ_ERR_INVALID_ARG, "wdl output needs a network with the WDL value head");
   if (B == 0) return AZ_OK;
   if (B > net->spec.max_batch) return fail(AZ_ERR_INVALID_ARG, "B = %d > max_batch %d", B, net->spec.max_batch);
   if (!planes || !legal || !policy || !value) return fail(AZ_ERR_INVALID_ARG, "NULL buffer");
   if (((uintptr_t)planes | (uintptr_t)legal | (uintptr_t)policy) & 15u)
     return fail(AZ_ERR_INVALID_ARG, "planes, legal and policy must be 16-byte aligned");
-  if ((uintptr_t)value & 3u) return fail(AZ_ERR_INVALID_ARG, "value must be 4-byte aligned");
+  if (((uintptr_t)value | (uintptr_t)wdl) & 3u) return fail(AZ_ERR_INVALID_ARG, "value and wdl must be 4-byte aligned");
   int cur = 0;
   hipError_t e = hipGetDevice(&cur);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (cur != net->device && (e = hipSetDevice(net->device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (net->dtype == AZ_F32)
+  if (dep)
+    e = az_launch_deployed(net->dtype, net->dn, planes, legal, B, policy, value, wdl, s);
+  else if (net->dtype == AZ_F32)
     e = az_launch_f32(net->dn, planes, legal, B, policy, value, s);
   else
     e = az_launch_mfma(net->dtype, choose_tiling(net, B), net->dn, planes, legal, B, policy, value, s);
@@ -438,9 +678,20 @@ int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_
   return AZ_OK;
 }
 
+int az_eval_batch(az_net* net, const float* planes, const uint8_t* legal, int32_t B, float* policy,
+                  float* value, void* stream) {
+  return az_eval_batch_wdl(net, planes, legal, B, policy, value, nullptr, stream);
+}
+
+int az_net_moves(const az_net* net) {
+  if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
+  return az_spec_moves(net->spec);
+}
+
 int az_net_set_tiling(az_net* net, int32_t tiling) {
   if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
-  if (net->dtype == AZ_F32 ? tiling != 0 : (tiling != 0 && !az_mfma_tiling_valid(net->spec.filters, tiling)))
+  const bool single = net->dtype == AZ_F32 || is_deployed(net->spec);
+  if (single ? tiling != 0 : (tiling != 0 && !az_mfma_tiling_valid(net->spec.filters, tiling)))
     return fail(AZ_ERR_INVALID_ARG, "tiling %d not available for this dtype", tiling);
   net->tiling = tiling;
   return AZ_OK;

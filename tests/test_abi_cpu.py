@@ -38,6 +38,56 @@ def test_weight_count_matches_layer_list():
     assert az.az_weight_count(az.make_spec(20, 2, 32, 73, 64, max_batch=1)) == 49451
     assert az.az_weight_count(az.make_spec(20, 24, 256, 73, 128, max_batch=1)) == 28397643
     assert az.az_weight_count(az.make_spec(20, 2, 32, 73, 64, max_batch=1, abi_version=7)) == 0
+    # the deployed network: 52 planes, 14 x 160 with pooling every second block,
+    # from-to head with 128-wide tokens, WDL head with 2 channels and 48 units
+    dep = azgen.DEPLOYED_14X160
+    assert az.az_weight_count(az.spec_from_shape(dep, 1)) == dep.weight_count() == 6255525
+
+
+def test_version1_spec_layout_is_accepted():
+    # a caller built against the first version passes only the first nine fields
+    v1 = az.az_layer_spec_v1(1, 20, 20, 128, 73, 128, 0, 0.0, 1)
+    ptr = ctypes.cast(ctypes.pointer(v1), ctypes.POINTER(az.az_layer_spec))
+    assert az.lib().az_weight_count(ptr) == 5944523
+
+
+def test_deployed_spec_validation_before_device():
+    dep = azgen.DEPLOYED_14X160
+    good = az.spec_from_shape(dep, 4)
+    blob = np.zeros(dep.weight_count(), np.float32)
+    ws = np.ones(2 * dep.blocks * dep.filters, np.float32)
+    acs = np.ones(2 * dep.blocks + 1, np.float32)
+
+    def spec(**kw):
+        s = az.spec_from_shape(dep, 4)
+        for k, v in kw.items():
+            setattr(s, k, v)
+        return s
+
+    def st(sp, dtype, ws_=None, acs_=None):
+        n = az.az_weight_count(sp)
+        return _load_status(sp, np.zeros(max(n, 1), np.float32), dtype, ws_, acs_)
+
+    # well-formed but not built: fp8 / f32, other widths, token width, head combinations
+    assert _load_status(good, blob, "fp8", ws, acs) == az.AZ_ERR_UNSUPPORTED
+    assert _load_status(good, blob, "f32") == az.AZ_ERR_UNSUPPORTED
+    assert st(spec(filters=128), "bf16") == az.AZ_ERR_UNSUPPORTED
+    assert st(spec(token_dim=64), "bf16") == az.AZ_ERR_UNSUPPORTED
+    assert st(spec(value_channels=33), "bf16") == az.AZ_ERR_UNSUPPORTED
+    assert st(spec(in_planes=65), "bf16") == az.AZ_ERR_UNSUPPORTED
+    assert st(spec(value_head=az.AZ_VALUE_TANH, value_channels=1), "bf16") == az.AZ_ERR_UNSUPPORTED
+    assert st(spec(policy_head=az.AZ_POLICY_PLANES, token_dim=0, policy_planes=73), "bf16") == az.AZ_ERR_UNSUPPORTED
+    planes_pool = az.make_spec(20, 2, 128, 73, 128, max_batch=4, pool_every=2)
+    assert st(planes_pool, "bf16") == az.AZ_ERR_UNSUPPORTED
+    # malformed
+    for bad in (spec(policy_planes=73), spec(token_dim=0), spec(value_channels=0), spec(policy_head=2),
+                spec(value_head=5), spec(pool_every=-1), spec(filters=162)):
+        assert az.az_weight_count(bad) == 0
+        assert _load_status(bad, blob, "bf16") == az.AZ_ERR_INVALID_ARG
+    # counts
+    assert _load_status(good, blob[:-1], "bf16") == az.AZ_ERR_INVALID_ARG
+    assert _load_status(good, blob, "int8", ws[:-1], acs) == az.AZ_ERR_INVALID_ARG
+    assert _load_status(good, blob, "int8") == az.AZ_ERR_INVALID_ARG
     assert az.az_weight_count(az.make_spec(20, 0, 32, 73, 64, max_batch=1)) == 0
 
 
@@ -63,7 +113,8 @@ def test_load_rejects_bad_arguments_before_device():
     assert "n_weights" in az.az_last_error()
     # malformed spec
     for bad in (az.make_spec(20, 2, 32, 73, 64, max_batch=0),
-                az.make_spec(20, 2, 32, 73, 64, max_batch=4, abi_version=2),
+                az.make_spec(20, 2, 32, 73, 64, max_batch=4, abi_version=3),
+                az.make_spec(20, 2, 32, 73, 64, max_batch=4, abi_version=0),
                 az.make_spec(20, 2, 32, 73, 64, value_conv_relu=3, max_batch=4),
                 az.make_spec(20, 2, 32, 73, 64, act_cap=-1.0, max_batch=4)):
         assert _load_status(bad, blob, "f32") == az.AZ_ERR_INVALID_ARG
@@ -97,6 +148,8 @@ def test_load_rejects_bad_arguments_before_device():
 
 def test_eval_and_free_reject_null_handle():
     assert az.az_eval_batch(None, 0, 0, 4, 0, 0, 0, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
+    assert az.az_eval_batch_wdl(None, 0, 0, 4, 0, 0, 0, 0, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
+    assert az.lib().az_net_moves(None) == az.AZ_ERR_INVALID_ARG
     assert az.az_net_set_tiling(None, 1, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
     assert az.az_net_device_bytes(None) == 0
     az.az_net_free(None)                                     # no-op

@@ -17,15 +17,26 @@ def _print(*a):
     print(*a, flush=True)
 
 
+def _scales(w, dtype):
+    if dtype == "f32":
+        return None, None
+    if w.shape.policy_head == "fromto":   # deployed network: fixed ReLU6 activation scale
+        from oracle import deployed as OD
+        blob = azgen.workload_weights(w)
+        return OD.weight_scales(w.shape, blob), np.full(2 * w.shape.blocks + 1, 6.0 / 127.0, np.float32)
+    return H.quant_scales(w.name, dtype)
+
+
 @pytest.mark.parametrize("use_graphs", [False, True])
-@pytest.mark.parametrize("wname,dtype", [("net20x128_int8_b1024", "int8"), ("tiny_2x32_f32_b16", "f32")])
+@pytest.mark.parametrize("wname,dtype", [("net20x128_int8_b1024", "int8"), ("tiny_2x32_f32_b16", "f32"),
+                                         ("deployed14x160_int8_b1024", "int8")])
 def test_pipeline_matches_eval_batch(wname, dtype, use_graphs):
     import torch
 
     import paper_2609_37447_amd as az
     w = W[wname]
     blob = azgen.workload_weights(w)
-    ws, acs = H.quant_scales(w.name, dtype) if dtype != "f32" else (None, None)
+    ws, acs = _scales(w, dtype)
     MB, SLOTS = 48, 3
     _print(f"case pipeline {wname} graphs={use_graphs} max_batch={MB} slots={SLOTS}")
     spec = az.spec_from_shape(w.shape, MB)
@@ -90,15 +101,16 @@ def _compact_definition(P, legal, K):
 
 
 @pytest.mark.parametrize("use_graphs", [False, True])
-def test_pipeline_compact_policy(use_graphs):
+@pytest.mark.parametrize("wname", ["net20x128_int8_b1024", "deployed14x160_int8_b1024"])
+def test_pipeline_compact_policy(use_graphs, wname):
     import torch
 
     import paper_2609_37447_amd as az
-    w = W["net20x128_int8_b1024"]
+    w = W[wname]
     blob = azgen.workload_weights(w)
-    ws, acs = H.quant_scales(w.name, "int8")
+    ws, acs = _scales(w, "int8")
     MB, K = 300, 48
-    _print(f"case pipeline compact int8 graphs={use_graphs} max_batch={MB} max_legal={K}")
+    _print(f"case pipeline compact {wname} graphs={use_graphs} max_batch={MB} max_legal={K}")
     spec = az.spec_from_shape(w.shape, MB)
     net = az.az_net_load(spec, blob, "int8", ws, acs)
     pipe = None
