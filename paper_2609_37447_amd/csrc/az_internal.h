@@ -60,7 +60,7 @@ struct AzDevNet {
   const float* emb_bc;     // [AZ_DEP_EMB_ROWS] row bias: be, then bv, then zeros
   const float* q_b;        // [D]
   const float* k_b;        // [D]
-  const double* pool_wt;   // per pooling block j (in block order): Wg^T as [2g][AZ_DEP_POOL_OPAD] fp64
+  const float* pool_wt;    // per pooling block (in block order): Wg as [2g/4][AZ_DEP_POOL_OPAD][4] fp32
   const float* pool_m;     // [2*blocks][F]: pooled-channel pre-activation scale (a[n]*s_w[n][f]; 1 for bf16)
   const float* pool_b;     // [2*blocks][F]: pooled-channel bias b1 (unscaled)
   const float* pool_cinv;  // [2*blocks]: factor of c in the regular channels (inv[n+1]; 1 for bf16)

@@ -27,8 +27,12 @@
 // over the wave; c (rounded to fp32) is then added to the regular channels in
 // the same epilogue that writes them.
 //
-// Heads.  The final tensor h (int8 codes, or bf16 hi + lo parts of the fp32
-// residual stream) feeds one bf16 GEMM whose rows are the 128 token rows and
+// bf16 networks carry the residual stream h as hi + lo: hi = bf16(h) is the
+// convolution operand in LDS, lo = bf16(h - hi) stays in the registers of the
+// lane that produces it (a 16-bit significand for the running sum).
+//
+// Heads.  The final tensor h (int8 codes, or the bf16 hi + lo parts) feeds one
+// bf16 GEMM whose rows are the 128 token rows and
 // the value rows.  The token, query and key products then run from registers:
 // each accumulator tile is split into bf16 hi + lo parts and used directly as
 // an MFMA operand, with the next weight matrix packed in the order the
@@ -112,22 +116,23 @@ struct DepCfg {
   static constexpr int BUF = 64 * RB;
   static constexpr int OFF_H = 0, OFF_T = BUF, OFF_Z = 2 * BUF;
   static constexpr int ZB = (RB + 256 + 255) / 256 * 256;
-  static constexpr int KSLOT = 2 * DF * 4;            // [bias F | qmul F] floats
+  static constexpr int KSLOT = 4 * DF * 4;            // [bias F | qmul F | pool m F | pool b F] floats
   static constexpr int OFF_K = OFF_Z + ZB;
   static constexpr int OFF_PG = OFF_K + 2 * KSLOT;    // pooled statistics, 2g doubles
   static constexpr int OFF_C = OFF_PG + 2 * DG * 8;   // projected biases, F floats
   static constexpr int TOWER_END = OFF_C + DF * 4;
-  static constexpr int OFF_X = BUF;                   // heads' bf16 input (int8: codes; bf16: lo part)
-  static constexpr int X_END = OFF_X + 64 * RBX;
+  static constexpr int OFF_X = BUF;                   // heads' bf16 input: the lo part (bf16 networks)
+  static constexpr int X_END = QUANT ? 0 : OFF_X + 64 * RBX;
   static constexpr int OFF_S = 0;                     // query-key logits [64][64] f32
   static constexpr int OFF_U = 64 * 64 * 4;           // value features [V][64] f32
   static constexpr int OFF_O = OFF_U + 32 * 64 * 4;   // promotion offsets [8][4] f32
   static constexpr int HEAD_END = OFF_O + 32 * 4;
-  static constexpr int SMEM = cmax(cmax(TOWER_END, X_END), HEAD_END);
+  static constexpr int OFF_HC = (cmax(cmax(TOWER_END, X_END), HEAD_END) + 15) & ~15;  // head constants
+  static constexpr int SMEM = OFF_HC + (2 * AZ_DEP_EMB_ROWS + 2 * DD) * 4;
   static_assert(OFF_T >= 64 * 128, "stem input fits in the T buffer");
   static constexpr int CPT = DF / T::KS;              // K steps per tap
   static constexpr int S = 9 * CPT;                   // K steps per layer
-  static constexpr int NBUF = QUANT ? 5 : 3;          // weight ring (steps), loaded NBUF-1 ahead
+  static constexpr int NBUF = 3;                      // weight ring (steps), loaded NBUF-1 ahead
   static_assert((2 * S) % NBUF == 0, "every block's first conv starts at ring slot 0");
   static constexpr int STEP_BYTES = DNMB * 64 * T::FB;
   static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
@@ -153,8 +158,10 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   const int Cin = p.in_planes;
   const float cap = p.act_cap;
 
-  // fp32 residual stream of the board (bf16 networks): [block][half][16]
-  float res[QUANT ? 1 : DNMB][QUANT ? 1 : 2][16];
+  // residual stream of the board (bf16 networks): h = hi + lo, hi = bf16(h) in
+  // the H buffer (the convolution operand), lo = bf16(h - hi) packed here, two
+  // per register: [block][half][run of 4 channels][2]
+  uint32_t rlo[QUANT ? 1 : DNMB][QUANT ? 1 : 2][QUANT ? 1 : 8];
 
   // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
   for (int i = lane; i < C::ZB / 16; i += 64)
@@ -187,19 +194,46 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
     for (int m = 0; m < DNMB; ++m) dst[m] = g_frag<MK>(src + m * 64 * T::FB);
   };
-  static_for<0, NBUF - 1>([&](auto i_c) {
-    constexpr int i = decltype(i_c)::value;
-    load_step(A[i], tw + (size_t)i * C::STEP_BYTES);
-  });
-  // per-layer epilogue constants [bias F | qmul F] of conv index k (0 = stem) into slot
-  auto stage_consts = [&](int slot, int k) {
-    float* dst = reinterpret_cast<float*>(smem + C::OFF_K + slot * C::KSLOT);
-    for (int i = lane; i < DF / 4; i += 64) {
-      reinterpret_cast<float4*>(dst)[i] = *reinterpret_cast<const float4*>(p.bias + (size_t)k * DF + 4 * i);
-      if (QUANT) reinterpret_cast<float4*>(dst + DF)[i] = *reinterpret_cast<const float4*>(p.qmul + (size_t)k * DF + 4 * i);
+  // per-layer epilogue constants [bias F | qmul F | pool m F | pool b F] of conv
+  // index k (0 = stem; the pooling constants of conv k - 1): lane-held float4s
+  // (10 floats per lane), loaded at the start of a layer and parked in LDS
+  // before its barrier
+  constexpr int KV = 4 * DF / 4;                     // float4s per slot
+  constexpr int KPL = (KV + 63) / 64;                // per lane
+  auto load_consts = [&](int k, float4(&dst)[KPL]) {
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) {
+      const int i = lane + 64 * t, arr = i / (DF / 4), off = 4 * (i % (DF / 4));
+      const float* src = arr == 0 ? p.bias + (size_t)k * DF
+                       : arr == 1 ? (QUANT ? p.qmul + (size_t)k * DF : p.bias)
+                       : arr == 2 ? p.pool_m + (size_t)(k - 1) * DF
+                                  : p.pool_b + (size_t)(k - 1) * DF;
+      dst[t] = i < KV ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  stage_consts(0, 1);
+  auto store_consts = [&](int slot, const float4(&v)[KPL]) {
+    float4* dst = reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT);
+#pragma unroll
+    for (int t = 0; t < KPL; ++t)
+      if (lane + 64 * t < KV) dst[lane + 64 * t] = v[t];
+  };
+  // head constants, staged once: embedding row scale and bias, query and key biases
+  {
+    float* hc = reinterpret_cast<float*>(smem + C::OFF_HC);
+    for (int i = lane; i < AZ_DEP_EMB_ROWS; i += 64) {
+      hc[i] = p.emb_sc[i];
+      hc[AZ_DEP_EMB_ROWS + i] = p.emb_bc[i];
+    }
+    for (int i = lane; i < DD; i += 64) {
+      hc[2 * AZ_DEP_EMB_ROWS + i] = p.q_b[i];
+      hc[2 * AZ_DEP_EMB_ROWS + DD + i] = p.k_b[i];
+    }
+  }
+  {
+    float4 k0[KPL];
+    load_consts(1, k0);
+    store_consts(0, k0);
+  }
   __syncthreads();
 
   // ---- stem: bf16 3x3 conv over 64 (padded) input channels, K = 576
@@ -207,39 +241,46 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     constexpr int SSTEP = DNMB * 64 * 16;  // bytes per K step of the stem stream
     const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)lane * 16;
     f32x16 sacc[DNMB][2];
-    bf16x8 a[2][DNMB];  // A fragments of K step st in a[st & 1], loaded one step ahead
-    auto load_step_s = [&](bf16x8(&dst)[DNMB], int st) {
+    // 36 K steps (tap = st / 4, 16 channels each): A fragments of step st in ring
+    // slot st % 4, loaded three steps ahead; B fragments one step ahead
+    constexpr int SR = 4, NST = 9 * DCP / 16;
+    bf16x8 a[SR][DNMB];
+    auto load_a = [&](int st) {
 #pragma unroll
-      for (int m = 0; m < DNMB; ++m) dst[m] = g_frag<MK_BF16>(sw8 + st * SSTEP + m * 64 * 16);
+      for (int m = 0; m < DNMB; ++m) a[st % SR][m] = g_frag<MK_BF16>(sw8 + st * SSTEP + m * 64 * 16);
     };
-    load_step_s(a[0], 0);
-#pragma unroll
-    for (int tap = 0; tap < 9; ++tap) {
-      const int dy = tap / 3 - 1, dx = tap % 3 - 1;
-      int row[2], sw[2];
+    auto load_b = [&](int st, bf16x8(&dst)[2]) {
+      const int tap = st / 4, cs = st % 4, dy = tap / 3 - 1, dx = tap % 3 - 1;
 #pragma unroll
       for (int n = 0; n < 2; ++n) {
         const int j = n * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
         const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
         const int src = r * 8 + c;
-        row[n] = ok ? OFF_T + src * 128 : OFF_Z + ((src * 128) & 255);
-        sw[n] = swz128(src);
+        const int row = ok ? OFF_T + src * 128 : OFF_Z + ((src * 128) & 255);
+        dst[n] = *reinterpret_cast<const bf16x8*>(smem + row + (((2 * cs + lhi) ^ swz128(src)) << 4));
       }
+    };
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int st = tap * 4 + s;
-        if (st + 1 < 36) load_step_s(a[(st + 1) & 1], st + 1);
-        bf16x8 bfr[2];
+    for (int st = 0; st < SR - 1; ++st) load_a(st);
+    bf16x8 bcur[2], bnext[2];
+    load_b(0, bcur);
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      if (st + SR - 1 < NST) load_a(st + SR - 1);
+      if (st + 1 < NST) load_b(st + 1, bnext);
+#pragma unroll
+      for (int m = 0; m < DNMB; ++m)
 #pragma unroll
         for (int n = 0; n < 2; ++n)
-          bfr[n] = *reinterpret_cast<const bf16x8*>(smem + row[n] + (((2 * s + lhi) ^ sw[n]) << 4));
-#pragma unroll
-        for (int m = 0; m < DNMB; ++m)
-#pragma unroll
-          for (int n = 0; n < 2; ++n)
-            sacc[m][n] = mma_bf16(a[st & 1][m], bfr[n], st == 0 ? f32x16{} : sacc[m][n]);
-      }
+          sacc[m][n] = mma_bf16(a[st % SR][m], bcur[n], st == 0 ? f32x16{} : sacc[m][n]);
+      bcur[0] = bnext[0];
+      bcur[1] = bnext[1];
     }
+    // the tower's first weight steps, in flight during the stem's epilogue
+    static_for<0, NBUF - 1>([&](auto i_c) {
+      constexpr int i = decltype(i_c)::value;
+      load_step(A[i], tw + (size_t)i * C::STEP_BYTES);
+    });
     // epilogue: bias, activation (codes for int8), store in the tower format at OFF_H
 #pragma unroll
     for (int m = 0; m < DNMB; ++m)
@@ -256,10 +297,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           if constexpr (!QUANT) {
             const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
             const float y2 = act_fn(v[4 * q + 2] + bb.z, cap), y3 = act_fn(v[4 * q + 3] + bb.w, cap);
-            res[m][n][4 * q + 0] = y0;
-            res[m][n][4 * q + 1] = y1;
-            res[m][n][4 * q + 2] = y2;
-            res[m][n][4 * q + 3] = y3;
+            rlo[m][n][2 * q + 0] = pack_bf16x2(y0 - bf16_round(y0), y1 - bf16_round(y1));
+            rlo[m][n][2 * q + 1] = pack_bf16x2(y2 - bf16_round(y2), y3 - bf16_round(y3));
             *reinterpret_cast<uint2*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi) =
                 make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
           } else {
@@ -297,6 +336,9 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       const int in_off = SECOND ? OFF_T : OFF_H;
       const int out_off = SECOND ? OFF_H : OFF_T;
       const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
+      // the next layer's epilogue constants, in flight during this layer
+      float4 kn[KPL];
+      if (has_next) load_consts(n_conv + 2, kn);
       // B fragments of one K step: rows of the current tap, chunk of channel step cs
       int row[2], sw[2], nrow[2], nsw[2];
       auto rows_for = [&](int tap, int(&rr)[2], int(&ss)[2]) {
@@ -381,42 +423,81 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       float cinv = 1.0f;
       if constexpr (POOL) {
         cinv = p.pool_cinv[n_conv];
-        double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
+        // (1) pooled activations to LDS as [pooled channel][square] f32 in the T
+        //     buffer (written by this layer's epilogue only afterwards); rows of
+        //     256 bytes with 16-byte chunks XOR-swizzled by the row
+        float* pt = reinterpret_cast<float*>(smem + OFF_T);
+        static_assert(DG * 64 * 4 <= C::BUF, "pooled activations fit in the T buffer");
         static_for<0, DNMB * 4>([&](auto k_c) {
           constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4;
           if constexpr (32 * m + 8 * q >= DFR) {
             const int ch0 = 32 * m + 8 * q + 4 * lhi;
-            const float4 mm = *reinterpret_cast<const float4*>(p.pool_m + (size_t)n_conv * DF + ch0);
-            const float4 bb = *reinterpret_cast<const float4*>(p.pool_b + (size_t)n_conv * DF + ch0);
+            const float4 mm = *reinterpret_cast<const float4*>(kslot + 2 * DF + ch0);
+            const float4 bb = *reinterpret_cast<const float4*>(kslot + 3 * DF + ch0);
             const float mv[4] = {mm.x, mm.y, mm.z, mm.w}, bv[4] = {bb.x, bb.y, bb.z, bb.w};
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const float p0 = med3(__builtin_fmaf((float)c[m][0][4 * q + r], mv[r], bv[r]), 0.0f, cap);
-              const float p1 = med3(__builtin_fmaf((float)c[m][1][4 * q + r], mv[r], bv[r]), 0.0f, cap);
-              double s = (double)p0 + (double)p1;
-              float mx = fmaxf(p0, p1);
+              const int pc = ch0 + r - DFR;
 #pragma unroll
-              for (int o = 1; o < 32; o <<= 1) {
-                s += shfl_xor_d(s, o);
-                mx = fmaxf(mx, __shfl_xor(mx, o));
-              }
-              if (l32 == 0) {
-                const int pc = ch0 + r - DFR;
-                pg[pc] = s * (1.0 / 64.0);
-                pg[DG + pc] = (double)mx;
+              for (int n = 0; n < 2; ++n) {
+                const int sq = 32 * n + l32;
+                pt[pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3)] =
+                    med3(__builtin_fmaf((float)c[m][n][4 * q + r], mv[r], bv[r]), 0.0f, cap);
               }
             }
           }
         });
         wave_lds_sync();
-        // lane L: outputs L and L + 64 (those below Fr)
-        const double* wt = p.pool_wt + (size_t)(n_conv / 2 / p.pool_every) * (2 * DG * AZ_DEP_POOL_OPAD);
+        // (2) lane pc < g: board sum (fp64) and maximum of its row; g = [mean, max]
+        double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
+        if (lane < DG) {
+          double sum = 0.0;
+          float mx = 0.0f;  // activations are >= 0
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const float4 v = *reinterpret_cast<const float4*>(pt + lane * 64 + ((j ^ (lane & 15)) << 2));
+            sum += (double)v.x;
+            sum += (double)v.y;
+            sum += (double)v.z;
+            sum += (double)v.w;
+            mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+          }
+          pg[lane] = sum * (1.0 / 64.0);
+          pg[DG + lane] = (double)mx;
+        }
+        wave_lds_sync();
+        // (3) c[o] = sum_i Wg[o][i] g[i] in fp64 (fp32 weights are exact): lane L
+        //     takes outputs L and L + 64; the weights, [i/4][o][4] floats, stream
+        //     in chunks of 16 inputs with the next chunk in flight
+        const float4* wt = reinterpret_cast<const float4*>(p.pool_wt) +
+                           (size_t)(n_conv / 2 / p.pool_every) * (2 * DG / 4) * AZ_DEP_POOL_OPAD;
+        constexpr int NCH = 2 * DG / 16;
+        float4 wbuf[2][2][4];
+        auto load_chunk = [&](float4(&dst)[2][4], int chk) {
+#pragma unroll
+          for (int k4 = 0; k4 < 4; ++k4) {
+            dst[0][k4] = wt[(size_t)(4 * chk + k4) * AZ_DEP_POOL_OPAD + lane];
+            dst[1][k4] = wt[(size_t)(4 * chk + k4) * AZ_DEP_POOL_OPAD + 64 + lane];
+          }
+        };
+        load_chunk(wbuf[0], 0);
         double c0 = 0.0, c1 = 0.0;
-#pragma unroll 8
-        for (int i = 0; i < 2 * DG; ++i) {
-          const double gi = pg[i];
-          c0 = __builtin_fma(wt[(size_t)i * AZ_DEP_POOL_OPAD + lane], gi, c0);
-          c1 = __builtin_fma(wt[(size_t)i * AZ_DEP_POOL_OPAD + 64 + lane], gi, c1);
+#pragma unroll
+        for (int chk = 0; chk < NCH; ++chk) {
+          if (chk + 1 < NCH) load_chunk(wbuf[(chk + 1) & 1], chk + 1);
+#pragma unroll
+          for (int k4 = 0; k4 < 4; ++k4) {
+            const float4 w0 = wbuf[chk & 1][0][k4], w1 = wbuf[chk & 1][1][k4];
+            const double* gi = pg + 16 * chk + 4 * k4;
+            c0 = __builtin_fma((double)w0.x, gi[0], c0);
+            c1 = __builtin_fma((double)w1.x, gi[0], c1);
+            c0 = __builtin_fma((double)w0.y, gi[1], c0);
+            c1 = __builtin_fma((double)w1.y, gi[1], c1);
+            c0 = __builtin_fma((double)w0.z, gi[2], c0);
+            c1 = __builtin_fma((double)w1.z, gi[2], c1);
+            c0 = __builtin_fma((double)w0.w, gi[3], c0);
+            c1 = __builtin_fma((double)w1.w, gi[3], c1);
+          }
         }
         float* cb = reinterpret_cast<float*>(smem + C::OFF_C);
         cb[lane] = (float)c0;
@@ -431,10 +512,12 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         hi = p.qhi[n_conv + 1];
         rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
       }
-      constexpr int NRUN = DNMB * 4, EP_AHEAD = QUANT ? 2 : 0, EP_RING = EP_AHEAD + 1;
-      constexpr bool RCODE = QUANT && SECOND;
+      constexpr int NRUN = DNMB * 4, EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
+      constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
+      constexpr bool RHI = !QUANT && SECOND;    // residual hi parts, read in place
       float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
       uint32_t rcode[RCODE ? EP_RING : 1][2];
+      uint2 rhi[RHI ? EP_RING : 1][2];
       auto ep_addr = [&](int m, int q, int n) {
         const int j = n * 32 + l32;
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
@@ -451,6 +534,10 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         if constexpr (RCODE) {
 #pragma unroll
           for (int n = 0; n < 2; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
+        }
+        if constexpr (RHI) {
+#pragma unroll
+          for (int n = 0; n < 2; ++n) rhi[slot][n] = *reinterpret_cast<const uint2*>(smem + ep_addr(m, q, n));
         }
       };
       static_for<0, EP_AHEAD>([&](auto k_c) { ep_load(k_c); });
@@ -473,14 +560,15 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
               y3 += cc.w;
             }
             if constexpr (SECOND) {
-              y0 = act_fn(y0 + res[m][n][4 * q + 0], cap);
-              y1 = act_fn(y1 + res[m][n][4 * q + 1], cap);
-              y2 = act_fn(y2 + res[m][n][4 * q + 2], cap);
-              y3 = act_fn(y3 + res[m][n][4 * q + 3], cap);
-              res[m][n][4 * q + 0] = y0;
-              res[m][n][4 * q + 1] = y1;
-              res[m][n][4 * q + 2] = y2;
-              res[m][n][4 * q + 3] = y3;
+              // block input h = hi + lo (exact in fp32)
+              const uint2 hv = rhi[slot][n];
+              const uint32_t l01 = rlo[m][n][2 * q], l23 = rlo[m][n][2 * q + 1];
+              y0 = act_fn(y0 + (__uint_as_float(hv.x << 16) + __uint_as_float(l01 << 16)), cap);
+              y1 = act_fn(y1 + (__uint_as_float(hv.x & 0xffff0000u) + __uint_as_float(l01 & 0xffff0000u)), cap);
+              y2 = act_fn(y2 + (__uint_as_float(hv.y << 16) + __uint_as_float(l23 << 16)), cap);
+              y3 = act_fn(y3 + (__uint_as_float(hv.y & 0xffff0000u) + __uint_as_float(l23 & 0xffff0000u)), cap);
+              rlo[m][n][2 * q + 0] = pack_bf16x2(y0 - bf16_round(y0), y1 - bf16_round(y1));
+              rlo[m][n][2 * q + 1] = pack_bf16x2(y2 - bf16_round(y2), y3 - bf16_round(y3));
             } else {
               y0 = act_fn(y0, cap);
               y1 = act_fn(y1, cap);
@@ -513,7 +601,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           }
         }
       });
-      if (has_next) stage_consts((n_conv + 1) & 1, n_conv + 2);
+      if (has_next) store_consts((n_conv + 1) & 1, kn);
       __syncthreads();
     };
 
@@ -525,21 +613,11 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     }
   }
 
-  // ---- heads input: bf16 rows [square][F] at OFF_X (int8: the final codes'
-  // values, exact; bf16: the low part h - bf16(h) of the fp32 residual, H
-  // holding bf16(h))
+  // ---- heads input (bf16 networks): the low part h - bf16(h) of the fp32
+  // residual as bf16 rows [square][F] at OFF_X, H holding bf16(h); int8
+  // networks read the final codes from H and convert them in registers
   using RX = Rot<C::RBX>;
-  if constexpr (QUANT) {
-    for (int idx = lane; idx < 64 * (DF / 8); idx += 64) {
-      const int k = idx % (DF / 8), sq = idx / (DF / 8);
-      const uint2 v = *reinterpret_cast<const uint2*>(smem + OFF_H + sq * RB + (R::pos(k >> 1, R::sw(sq)) << 4) + (k & 1) * 8);
-      const uint4 o = make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
-                                 pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
-                                 pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
-                                 pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y)));
-      *reinterpret_cast<uint4*>(smem + C::OFF_X + sq * C::RBX + (RX::pos(k, RX::sw(sq)) << 4)) = o;
-    }
-  } else {
+  if constexpr (!QUANT) {
 #pragma unroll
     for (int m = 0; m < DNMB; ++m)
 #pragma unroll
@@ -548,11 +626,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
         for (int n = 0; n < 2; ++n) {
           const int j = n * 32 + l32;
-          float lo[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) lo[r] = res[m][n][4 * q + r] - bf16_round(res[m][n][4 * q + r]);
           *reinterpret_cast<uint2*>(smem + C::OFF_X + j * C::RBX + (RX::pos(ch0 >> 3, RX::sw(j)) << 4) + 8 * lhi) =
-              make_uint2(pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]));
+              make_uint2(rlo[m][n][2 * q], rlo[m][n][2 * q + 1]);
         }
       }
   }
@@ -563,18 +638,35 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   f32x16 uacc[2];       // value rows 128..159
   {
     const uint8_t* ew = static_cast<const uint8_t*>(p.emb_w) + (size_t)lane * 16;
+    // A fragments of K step s in ring slot s % 4, loaded three steps ahead
+    constexpr int ES = DF / 16, ER = 4;
+    bf16x8 awr[ER][DEMB];
+    auto load_e = [&](int st) {
 #pragma unroll
-    for (int s = 0; s < DF / 16; ++s) {
-      bf16x8 aw[DEMB];
+      for (int m = 0; m < DEMB; ++m) awr[st % ER][m] = g_frag<MK_BF16>(ew + (st * DEMB + m) * 64 * 16);
+    };
 #pragma unroll
-      for (int m = 0; m < DEMB; ++m) aw[m] = g_frag<MK_BF16>(ew + (s * DEMB + m) * 64 * 16);
+    for (int st = 0; st < ER - 1; ++st) load_e(st);
+#pragma unroll
+    for (int s = 0; s < ES; ++s) {
+      if (s + ER - 1 < ES) load_e(s + ER - 1);
+      const bf16x8(&aw)[DEMB] = awr[s % ER];
       bf16x8 bx[2], bh[2];
 #pragma unroll
       for (int n = 0; n < 2; ++n) {
         const int j = n * 32 + l32;
-        bx[n] = *reinterpret_cast<const bf16x8*>(smem + C::OFF_X + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
-        if constexpr (!QUANT)
+        if constexpr (QUANT) {
+          // eight codes of channels 16 s + 8 lhi .. + 7, exact in bf16
+          const uint2 v = *reinterpret_cast<const uint2*>(smem + OFF_H + j * RB + (R::pos(s, R::sw(j)) << 4) + 8 * lhi);
+          bx[n] = __builtin_bit_cast(
+              bf16x8, make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
+                                 pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
+                                 pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
+                                 pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y))));
+        } else {
+          bx[n] = *reinterpret_cast<const bf16x8*>(smem + C::OFF_X + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
           bh[n] = *reinterpret_cast<const bf16x8*>(smem + OFF_H + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+        }
       }
 #pragma unroll
       for (int n = 0; n < 2; ++n) {
@@ -591,14 +683,15 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   __syncthreads();  // H and X are dead from here on
 
   // token values relu(acc * scale + bias); value features u[c][sq] to LDS
+  const float* HC = reinterpret_cast<const float*>(smem + C::OFF_HC);
   {
 #pragma unroll
     for (int m = 0; m < DTB; ++m)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
         const int r0 = 32 * m + 8 * jq + 4 * lhi;
-        const float4 sc = *reinterpret_cast<const float4*>(p.emb_sc + r0);
-        const float4 bc = *reinterpret_cast<const float4*>(p.emb_bc + r0);
+        const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+        const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
         const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
 #pragma unroll
         for (int n = 0; n < 2; ++n)
@@ -610,8 +703,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
     for (int jq = 0; jq < 4; ++jq) {
       const int r0 = DD + 8 * jq + 4 * lhi;
-      const float4 sc = *reinterpret_cast<const float4*>(p.emb_sc + r0);
-      const float4 bc = *reinterpret_cast<const float4*>(p.emb_bc + r0);
+      const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+      const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
       const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -644,14 +737,23 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   {
     const uint8_t* qp = static_cast<const uint8_t*>(p.q_w) + (size_t)lane * 16;
     const uint8_t* kp = static_cast<const uint8_t*>(p.k_w) + (size_t)lane * 16;
-#pragma unroll
-    for (int s = 0; s < DD / 16; ++s) {
-      bf16x8 aq[DTB], ak[DTB];
+    // A fragments of K step s in ring slot s % 2, loaded one step ahead
+    constexpr int QS = DD / 16, QR = 2;
+    bf16x8 aqr[QR][DTB], akr[QR][DTB];
+    auto load_qk = [&](int st) {
 #pragma unroll
       for (int m = 0; m < DTB; ++m) {
-        aq[m] = g_frag<MK_BF16>(qp + (s * DTB + m) * 64 * 16);
-        ak[m] = g_frag<MK_BF16>(kp + (s * DTB + m) * 64 * 16);
+        aqr[st % QR][m] = g_frag<MK_BF16>(qp + (st * DTB + m) * 64 * 16);
+        akr[st % QR][m] = g_frag<MK_BF16>(kp + (st * DTB + m) * 64 * 16);
       }
+    };
+#pragma unroll
+    for (int st = 0; st < QR - 1; ++st) load_qk(st);
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      if (s + QR - 1 < QS) load_qk(s + QR - 1);
+      const bf16x8(&aq)[DTB] = aqr[s % QR];
+      const bf16x8(&ak)[DTB] = akr[s % QR];
 #pragma unroll
       for (int n = 0; n < 2; ++n) {
         bf16x8 xh, xl;
@@ -670,8 +772,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
         const int r0 = 32 * m + 8 * jq + 4 * lhi;
-        const float4 bq = *reinterpret_cast<const float4*>(p.q_b + r0);
-        const float4 bk = *reinterpret_cast<const float4*>(p.k_b + r0);
+        const float4 bq = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + r0);
+        const float4 bk = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + DD + r0);
         const float qv[4] = {bq.x, bq.y, bq.z, bq.w}, kv[4] = {bk.x, bk.y, bk.z, bk.w};
 #pragma unroll
         for (int n = 0; n < 2; ++n)
@@ -685,9 +787,28 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
   // S[f][t] = sum_d Q[f][d] K[t][d] (hi*hi + hi*lo + lo*hi) and the promotion
   // offsets O^T[k][t] = sum_d Wp[k][d] K[t][d] for the last row's destinations
+  // action table entries and legal-mask words of the softmax, in flight
+  // during the query-key products
+  constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
+  uint4 tbl[NIT];
+  uint32_t mkw[NIT];
+  {
+    const uint8_t* lg = legal + (size_t)b * NA;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      const bool in = a0 < NA;
+      tbl[i] = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
+      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
+      mkw[i] = in ? mk0 : 0u;
+    }
+  }
   f32x16 Sa[2][2], Oa;
   {
     const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
+    bf16x8 apw[DD / 16];  // every K step's promotion-weight fragment, loaded up front
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) apw[s] = g_frag<MK_BF16>(pw + s * 64 * 16);
 #pragma unroll
     for (int s = 0; s < DD / 16; ++s) {
       bf16x8 qh[2], ql[2], kh[2], kl[2];
@@ -704,9 +825,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           Sa[mf][nt] = mma_bf16(qh[mf], kl[nt], Sa[mf][nt]);
           Sa[mf][nt] = mma_bf16(ql[mf], kh[nt], Sa[mf][nt]);
         }
-      const bf16x8 aw = g_frag<MK_BF16>(pw + s * 64 * 16);
-      Oa = mma_bf16(aw, kh[1], s == 0 ? f32x16{} : Oa);
-      Oa = mma_bf16(aw, kl[1], Oa);
+      Oa = mma_bf16(apw[s], kh[1], s == 0 ? f32x16{} : Oa);
+      Oa = mma_bf16(apw[s], kl[1], Oa);
     }
   }
   // logits pre-scaled by log2(e) for the exp2 softmax
@@ -733,19 +853,16 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
   // ---- legal-action softmax: lane owns the runs of 4 actions at 256 i + 4 lane
   {
-    constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
     const float* S = reinterpret_cast<const float*>(smem + C::OFF_S);
     const float* O = reinterpret_cast<const float*>(smem + C::OFF_O);
-    const uint8_t* lg = legal + (size_t)b * NA;
     float e[NIT][4];
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NIT; ++i) {
       const int a0 = 256 * i + 4 * lane;
       const bool in = a0 < NA;  // NA is a multiple of 4
-      const uint4 tb = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
-      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
-      const uint32_t mk = in ? mk0 : 0u;
+      const uint4 tb = tbl[i];
+      const uint32_t mk = mkw[i];
       const uint32_t te[4] = {tb.x, tb.y, tb.z, tb.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -787,7 +904,22 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       const bool ok = k < H;
       const int kk = ok ? k : 0;
       float y = p.wdl_fc1_b[kk];
-      for (int i = 0; i < NU; ++i) y = __builtin_fmaf(p.wdl_fc1_t[(size_t)i * H + kk], U[i], y);
+      // fc1 row of unit kk in chunks of 16 inputs, the next chunk in flight
+      // (NU is a multiple of 64)
+      float wa[16], wb[16];
+      auto ld = [&](float(&d)[16], int i0) {
+#pragma unroll
+        for (int t = 0; t < 16; ++t) d[t] = p.wdl_fc1_t[(size_t)(i0 + t) * H + kk];
+      };
+      ld(wa, 0);
+      for (int i0 = 0; i0 < NU; i0 += 32) {
+        ld(wb, i0 + 16);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wa[t], U[i0 + t], y);
+        if (i0 + 32 < NU) ld(wa, i0 + 32);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wb[t], U[i0 + 16 + t], y);
+      }
       y = ok ? fmaxf(y, 0.0f) : 0.0f;
       z0 = __builtin_fmaf(p.wdl_fc2_w[kk], y, z0);
       z1 = __builtin_fmaf(p.wdl_fc2_w[H + kk], y, z1);

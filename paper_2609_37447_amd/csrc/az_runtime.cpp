@@ -419,7 +419,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   std::vector<uint8_t> stem, tower, head, emb, qw, kw, pw;
   std::vector<float> bias, qmul, qres, qhi, head_b, fc2w, head_sc, head_bc, fc1t;
   std::vector<float> emb_sc, emb_bc, pool_m, pool_b, pool_cinv, wfc1t;
-  std::vector<double> pool_wt;
+  std::vector<float> pool_wt;
   std::vector<uint32_t> actions;
   const float hs = quant ? act_scales[2 * NB] : 1.0f;
   try {
@@ -523,11 +523,14 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
             if (quant) pool_m[(size_t)n * F + f] = act_scales[n] * w_scales[(size_t)n * F + f];
           }
           if (quant) pool_cinv[n] = (float)(1.0 / (double)act_scales[n + 1]);
-          // Wg^T in fp64, outputs padded to AZ_DEP_POOL_OPAD
+          // Wg as [2g/4][AZ_DEP_POOL_OPAD][4] (outputs padded with zeros): lane o of
+          // a wave loads Wg[o][4s .. 4s+3] at ((s * OPAD + o) * 4), so the wave's
+          // float4 loads are contiguous
           const size_t base = pool_wt.size();
-          pool_wt.resize(base + (size_t)2 * g * AZ_DEP_POOL_OPAD, 0.0);
+          pool_wt.resize(base + (size_t)2 * g * AZ_DEP_POOL_OPAD, 0.0f);
           for (int i = 0; i < 2 * g; ++i)
-            for (int o = 0; o < Fr; ++o) pool_wt[base + (size_t)i * AZ_DEP_POOL_OPAD + o] = v.pool[j][(size_t)o * 2 * g + i];
+            for (int o = 0; o < Fr; ++o)
+              pool_wt[base + ((size_t)(i / 4) * AZ_DEP_POOL_OPAD + o) * 4 + i % 4] = v.pool[j][(size_t)o * 2 * g + i];
         }
         // embedding: D token rows (We) then V value rows (Wv), K = F, plain K order
         std::vector<float> E((size_t)AZ_DEP_EMB_ROWS * F, 0.0f);
@@ -573,7 +576,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
       {emb.data(), emb.size(), 0}, {qw.data(), qw.size(), 0}, {kw.data(), kw.size(), 0},
       {pw.data(), pw.size(), 0}, {emb_sc.data(), emb_sc.size() * 4, 0}, {emb_bc.data(), emb_bc.size() * 4, 0},
       {dep ? v.q_b : nullptr, dep ? (size_t)D * 4 : 0, 0}, {dep ? v.k_b : nullptr, dep ? (size_t)D * 4 : 0, 0},
-      {pool_wt.data(), pool_wt.size() * 8, 0}, {pool_m.data(), pool_m.size() * 4, 0},
+      {pool_wt.data(), pool_wt.size() * 4, 0}, {pool_m.data(), pool_m.size() * 4, 0},
       {pool_b.data(), pool_b.size() * 4, 0}, {pool_cinv.data(), pool_cinv.size() * 4, 0},
       {actions.data(), actions.size() * 4, 0}, {wfc1t.data(), wfc1t.size() * 4, 0}};
   size_t total = 0;
@@ -636,7 +639,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
     d.emb_bc = atf(19);
     d.q_b = atf(20);
     d.k_b = atf(21);
-    d.pool_wt = reinterpret_cast<const double*>(at(22));
+    d.pool_wt = atf(22);
     d.pool_m = atf(23);
     d.pool_b = atf(24);
     d.pool_cinv = atf(25);
