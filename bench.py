@@ -49,8 +49,10 @@ def kernel_source(shape):
 # for the kernel source it was taken on only: any other source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {  # (workload, tiling): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    ("net20x128_int8_b1024", 3): ("b9bd3d55db80720f503d375e8be1c48f5f2e42261548b86b1ec53f53c647a5e2",
-                                  32097.4, 18704.0),
+    ("net20x128_int8_b1024", 3): ("94a0de94aaa0eef2e0bcb9398aa55cff0e38e3f2fc36dc854802da5a70803d0a",
+                                  32044.8, 18704.0),
+    ("deployed14x160_int8_b1024", 0): ("980e03fbb97b6b5e7c09f0387c587ef848c594f80146bd7ee44554172088b0c2",
+                                       45325.1, 24704.0),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
