@@ -230,6 +230,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="net20x128_int8_b1024", choices=sorted(azgen.WORKLOADS))
     ap.add_argument("--tiling", type=int, default=0, choices=(0, 1, 2, 3))
+    ap.add_argument("--batch", type=int, default=0,
+                    help="evaluate this many positions per step instead of the workload's batch "
+                         "(e.g. 64 for the interactive regime: one outstanding batch of 64)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay measurement")
@@ -250,8 +253,8 @@ def main():
     w = azgen.WORKLOADS[args.workload]
     blob = azgen.workload_weights(w)
     ws, acs = load_scales(w)
-    planes, legal = azgen.make_inputs(w)
-    B = w.batch
+    B = args.batch or w.batch
+    planes, legal = azgen.make_inputs(w, n=B)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     net = az.az_net_load(az.spec_from_shape(w.shape, B), blob, w.dtype, ws, acs)
@@ -323,7 +326,7 @@ def main():
         torch.cuda.synchronize()
         graph_us = g0.elapsed_time(g1) * 1000.0 / n_rep
         del g
-    pipeline = None if args.no_pipeline else pipeline_rates(az, net, w, planes, legal, args.steps)
+    pipeline = None if (args.no_pipeline or B != w.batch) else pipeline_rates(az, net, w, planes, legal, args.steps)
     az.az_net_free(net)
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)
@@ -349,7 +352,7 @@ def main():
                    "params": w.shape.weight_count(), "flop_per_position": flop_pos},
         "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_bytes(w, tiling), "traffic_unit": "bytes per launch"},
+                     "traffic": traffic_bytes(w, tiling) if B == w.batch else None, "traffic_unit": "bytes per launch"},
         "latency_us": {"p10": float(np.percentile(lat, 10)), "p50": float(np.percentile(lat, 50)),
                        "p90": float(np.percentile(lat, 90)), "calls": int(lat.size)},
         "graph_replay_us": graph_us,

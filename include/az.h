@@ -292,16 +292,16 @@ int az_compare_outputs(const float* policy_ref, const float* value_ref, const fl
 typedef struct az_pipeline az_pipeline;
 
 /* Creates a pipeline on the handle's device.  max_batch: 1..the handle's
- * max_batch; slots: 1..64; flags: an OR of AZ_PIPE_*; max_legal: 1..P*64 with
- * AZ_PIPE_COMPACT_POLICY, else 0.  Allocates all buffers (pinned host memory
+ * max_batch; slots: 1..64; flags: an OR of AZ_PIPE_*; max_legal: 1..n_moves
+ * (az_net_moves) with AZ_PIPE_COMPACT_POLICY, else 0.  Allocates all buffers (pinned host memory
  * with hipHostMalloc, device memory, streams, events); nothing leaks on
  * failure.  Returns AZ_OK, AZ_ERR_INVALID_ARG, AZ_ERR_NOMEM or AZ_ERR_DEVICE. */
 int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t flags, int32_t max_legal,
                        az_pipeline** out);
 
 /* Host buffers of a slot (any output pointer may be NULL): planes
- * [max_batch][in_planes][8][8] f32 and legal [max_batch][P*64] u8 (inputs);
- * value [max_batch] f32 and policy (outputs): [max_batch][P*64] f32, or with
+ * [max_batch][in_planes][8][8] f32 and legal [max_batch][n_moves] u8 (inputs);
+ * value [max_batch] f32 and policy (outputs): [max_batch][n_moves] f32, or with
  * AZ_PIPE_COMPACT_POLICY [max_batch][max_legal] f32 plus legal_count
  * [max_batch] i32 (NULL without the flag).  The pipeline owns them; they stay
  * valid until az_pipeline_free.  Do not touch a slot's buffers between its
