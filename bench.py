@@ -41,7 +41,7 @@ def is_deployed(shape):
 
 
 def kernel_source(shape):
-    return os.path.join(CSRC, "az_kernels_deployed.hip" if is_deployed(shape) else "az_kernels_mfma.hip")
+    return os.path.join(CSRC, "az_dep_kernel.h" if is_deployed(shape) else "az_kernels_mfma.hip")
 
 # HBM traffic of the fused kernel from rocprofv3 --pmc passes (FETCH_SIZE, then
 # WRITE_SIZE, KiB per dispatch), scaled by what the same counters read for a plain

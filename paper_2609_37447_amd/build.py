@@ -21,8 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libaz_mi355x.so")
 
-SOURCES = ["az_runtime.cpp", "az_kernels_f32.hip", "az_kernels_mfma.hip", "az_kernels_deployed.hip",
-           "az_compare.hip", "az_pipeline.hip"]
+SOURCES = ["az_runtime.cpp", "az_kernels_f32.hip", "az_kernels_mfma.hip", "az_kernels_deployed_int8.hip",
+           "az_kernels_deployed_bf16.hip", "az_compare.hip", "az_pipeline.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall",

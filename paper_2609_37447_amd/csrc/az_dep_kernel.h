@@ -4,11 +4,14 @@
 // outputs", Section 4.3 "Convolution, attention, and global context", "Three
 // policy representations", "Value and training-only heads", Appendix D).
 //
-// One workgroup is one wave and evaluates one board end to end; four such
-// workgroups share a compute unit (int8), one per SIMD.  The wave owns every
-// output channel (five 32-channel MFMA blocks) and both half-board square
-// blocks of every layer, so global pooling, the heads and both softmaxes need
-// no exchange with other waves.
+// One workgroup evaluates one board end to end.  With one wave per board (the
+// default from ~a quarter of the chip's boards up), four such workgroups share a
+// compute unit (int8), one per SIMD, and the wave owns every output tile: five
+// 32-channel MFMA blocks times both half-board square blocks, so global pooling,
+// the heads and both softmaxes need no exchange with other waves.  For small
+// batches, whose boards do not fill the chip, two waves share a board: each owns
+// one half-board square block of every layer, the pooled statistics meet in
+// LDS, and the heads run in the first wave.
 //
 // Tower.  Every 3x3 convolution is an implicit GEMM D[ch][sq] = sum_k
 // W[ch][k] X[k][sq], k = tap * C + c, with weights as the A operand (streamed
@@ -40,6 +43,8 @@
 // applied to both operands of the product).  Query-key logits are written to
 // LDS once, gathered through the action table, and soft-maxed over the legal
 // actions in fp32; the WDL head runs on the vector ALUs.
+#pragma once
+
 #include "az_internal.h"
 #include "az_mfma_common.h"
 
@@ -78,10 +83,17 @@ struct Rot {
 // swizzle of a 128-byte row (the stem's 64 bf16 input channels)
 __device__ __forceinline__ int swz128(int sq) { return (sq >> 1) & 7; }
 
+// LDS writes before, reads after, across every wave of the workgroup
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+// the same ordering within one wave (LDS writes by its lanes, reads by others)
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // bf16 hi and lo parts of eight fp32 values: x = hi + lo within 2^-16 |x|.
@@ -138,8 +150,12 @@ struct DepCfg {
   static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
 };
 
-template <int MK>
-__global__ __attribute__((amdgpu_flat_work_group_size(64, 64), amdgpu_waves_per_eu(1, 1))) void
+// NWB waves per board (one workgroup per board): 1 (every output tile of the
+// board in one wave; four boards per compute unit) or 2 (the two half-board
+// square blocks in two waves, for small batches whose boards do not fill the
+// chip; the heads then run in the first wave).
+template <int MK, int NWB>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * NWB, 64 * NWB), amdgpu_waves_per_eu(1, 1))) void
 az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal,
               float* __restrict__ policy, float* __restrict__ value, float* __restrict__ wdl) {
   using C = DepCfg<MK>;
@@ -152,7 +168,12 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[C::SMEM];
 
-  const int lane = threadIdx.x;
+  static_assert(NWB == 1 || NWB == 2, "waves per board");
+  constexpr int NBW = 2 / NWB;  // half-board square blocks per wave
+  constexpr int NT = 64 * NWB;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wn = NWB == 1 ? 0 : __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = wn * NBW;      // the wave's first square block
   const int l32 = lane & 31, lhi = lane >> 5;
   const int b = blockIdx.x;
   const int Cin = p.in_planes;
@@ -161,38 +182,48 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // residual stream of the board (bf16 networks): h = hi + lo, hi = bf16(h) in
   // the H buffer (the convolution operand), lo = bf16(h - hi) packed here, two
   // per register: [block][half][run of 4 channels][2]
-  uint32_t rlo[QUANT ? 1 : DNMB][QUANT ? 1 : 2][QUANT ? 1 : 8];
+  uint32_t rlo[QUANT ? 1 : DNMB][QUANT ? 1 : NBW][QUANT ? 1 : 8];
 
   // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
-  for (int i = lane; i < C::ZB / 16; i += 64)
+  for (int i = tid; i < C::ZB / 16; i += NT)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
-  for (int i = lane; i < DF; i += 64) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
+  for (int i = tid; i < DF; i += NT) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
   {
-    // item k = planes 8k..8k+7: lane = square, eight coalesced loads, one 16-byte store
-    float pv[DCP / 8][8];
+    // item k = planes 8k..8k+7 (wave wn takes k = wn, wn + NWB, ...): lane =
+    // square, eight coalesced loads, one 16-byte store
+    constexpr int KI = DCP / 8 / NWB;
+    float pv[KI][8];
 #pragma unroll
-    for (int k = 0; k < DCP / 8; ++k)
+    for (int ki = 0; ki < KI; ++ki)
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
-        const int c = 8 * k + t;
+        const int c = 8 * (wn + NWB * ki) + t;
         const bool ok = c < Cin;
         const float x = planes[((size_t)b * Cin + (ok ? c : 0)) * 64 + lane];
-        pv[k][t] = ok ? x : 0.0f;
+        pv[ki][t] = ok ? x : 0.0f;
       }
 #pragma unroll
-    for (int k = 0; k < DCP / 8; ++k)
+    for (int ki = 0; ki < KI; ++ki) {
+      const int k = wn + NWB * ki;
       *reinterpret_cast<uint4*>(smem + OFF_T + lane * 128 + ((k ^ swz128(lane)) << 4)) =
-          make_uint4(pack_bf16x2(pv[k][0], pv[k][1]), pack_bf16x2(pv[k][2], pv[k][3]),
-                     pack_bf16x2(pv[k][4], pv[k][5]), pack_bf16x2(pv[k][6], pv[k][7]));
+          make_uint4(pack_bf16x2(pv[ki][0], pv[ki][1]), pack_bf16x2(pv[ki][2], pv[ki][3]),
+                     pack_bf16x2(pv[ki][4], pv[ki][5]), pack_bf16x2(pv[ki][6], pv[ki][7]));
+    }
   }
 
-  // tower weight ring: K step i of the stream lives in A[i % NBUF]
+  // tower weight ring: K step i of the stream lives in A[i % NBUF].  The stream
+  // is read through a buffer resource: the lane's offset is a constant VGPR, the
+  // step's byte offset a scalar and the block's a literal, so a step's five
+  // loads cost no vector address arithmetic.
   constexpr int NBUF = C::NBUF;
-  const uint8_t* tw = static_cast<const uint8_t*>(p.tower_w) + (size_t)lane * T::FB;
+  const __amdgpu_buffer_rsrc_t twr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.tower_w), (short)0, (int)(2 * p.blocks * C::LAYER_BYTES), 0x00020000);
+  const int tvoff = lane * T::FB;
   frag_t A[NBUF][DNMB];
-  auto load_step = [&](frag_t(&dst)[DNMB], const uint8_t* src) {
+  auto load_step = [&](frag_t(&dst)[DNMB], int soff) {
 #pragma unroll
-    for (int m = 0; m < DNMB; ++m) dst[m] = g_frag<MK>(src + m * 64 * T::FB);
+    for (int m = 0; m < DNMB; ++m)
+      dst[m] = __builtin_bit_cast(frag_t, __builtin_amdgcn_raw_buffer_load_b128(twr, tvoff, soff + m * 64 * T::FB, 0));
   };
   // per-layer epilogue constants [bias F | qmul F | pool m F | pool b F] of conv
   // index k (0 = stem; the pooling constants of conv k - 1): lane-held float4s
@@ -211,7 +242,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       dst[t] = i < KV ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  auto store_consts = [&](int slot, const float4(&v)[KPL]) {
+  auto store_consts = [&](int slot, const float4(&v)[KPL]) {  // by the first wave
     float4* dst = reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT);
 #pragma unroll
     for (int t = 0; t < KPL; ++t)
@@ -220,16 +251,16 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // head constants, staged once: embedding row scale and bias, query and key biases
   {
     float* hc = reinterpret_cast<float*>(smem + C::OFF_HC);
-    for (int i = lane; i < AZ_DEP_EMB_ROWS; i += 64) {
+    for (int i = tid; i < AZ_DEP_EMB_ROWS; i += NT) {
       hc[i] = p.emb_sc[i];
       hc[AZ_DEP_EMB_ROWS + i] = p.emb_bc[i];
     }
-    for (int i = lane; i < DD; i += 64) {
+    for (int i = tid; i < DD; i += NT) {
       hc[2 * AZ_DEP_EMB_ROWS + i] = p.q_b[i];
       hc[2 * AZ_DEP_EMB_ROWS + DD + i] = p.k_b[i];
     }
   }
-  {
+  if (wn == 0) {
     float4 k0[KPL];
     load_consts(1, k0);
     store_consts(0, k0);
@@ -240,7 +271,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   {
     constexpr int SSTEP = DNMB * 64 * 16;  // bytes per K step of the stem stream
     const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)lane * 16;
-    f32x16 sacc[DNMB][2];
+    f32x16 sacc[DNMB][NBW];
     // 36 K steps (tap = st / 4, 16 channels each): A fragments of step st in ring
     // slot st % 4, loaded three steps ahead; B fragments one step ahead
     constexpr int SR = 4, NST = 9 * DCP / 16;
@@ -249,11 +280,11 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
       for (int m = 0; m < DNMB; ++m) a[st % SR][m] = g_frag<MK_BF16>(sw8 + st * SSTEP + m * 64 * 16);
     };
-    auto load_b = [&](int st, bf16x8(&dst)[2]) {
+    auto load_b = [&](int st, bf16x8(&dst)[NBW]) {
       const int tap = st / 4, cs = st % 4, dy = tap / 3 - 1, dx = tap % 3 - 1;
 #pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        const int j = n * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
+      for (int n = 0; n < NBW; ++n) {
+        const int j = (n0 + n) * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
         const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
         const int src = r * 8 + c;
         const int row = ok ? OFF_T + src * 128 : OFF_Z + ((src * 128) & 255);
@@ -262,7 +293,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     };
 #pragma unroll
     for (int st = 0; st < SR - 1; ++st) load_a(st);
-    bf16x8 bcur[2], bnext[2];
+    bf16x8 bcur[NBW], bnext[NBW];
     load_b(0, bcur);
 #pragma unroll
     for (int st = 0; st < NST; ++st) {
@@ -271,15 +302,15 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 #pragma unroll
       for (int m = 0; m < DNMB; ++m)
 #pragma unroll
-        for (int n = 0; n < 2; ++n)
+        for (int n = 0; n < NBW; ++n)
           sacc[m][n] = mma_bf16(a[st % SR][m], bcur[n], st == 0 ? f32x16{} : sacc[m][n]);
-      bcur[0] = bnext[0];
-      bcur[1] = bnext[1];
+#pragma unroll
+      for (int n = 0; n < NBW; ++n) bcur[n] = bnext[n];
     }
     // the tower's first weight steps, in flight during the stem's epilogue
     static_for<0, NBUF - 1>([&](auto i_c) {
       constexpr int i = decltype(i_c)::value;
-      load_step(A[i], tw + (size_t)i * C::STEP_BYTES);
+      load_step(A[i], i * C::STEP_BYTES);
     });
     // epilogue: bias, activation (codes for int8), store in the tower format at OFF_H
 #pragma unroll
@@ -291,8 +322,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
         if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
 #pragma unroll
-        for (int n = 0; n < 2; ++n) {
-          const int j = n * 32 + l32;
+        for (int n = 0; n < NBW; ++n) {
+          const int j = (n0 + n) * 32 + l32;
           const f32x16& v = sacc[m][n];
           if constexpr (!QUANT) {
             const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
@@ -318,7 +349,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // ---- residual tower
   {
     constexpr int CPT = C::CPT;
-    acc_t c[DNMB][2];
+    acc_t c[DNMB][NBW];
     const int nconv = 2 * p.blocks;
 
     const int l32_ = l32, lhi_ = lhi;
@@ -331,44 +362,61 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       // hoisted out of the block loop and held (or spilled) across it
       int l32 = l32_, lhi = lhi_;
       asm volatile("" : "+v"(l32), "+v"(lhi));
-      const uint8_t* wl = tw + (size_t)n_conv * C::LAYER_BYTES;
+      const int wl = n_conv * (int)C::LAYER_BYTES;  // byte offset of the layer in the stream
       const bool has_next = n_conv + 1 < nconv;
       const int in_off = SECOND ? OFF_T : OFF_H;
       const int out_off = SECOND ? OFF_H : OFF_T;
       const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
       // the next layer's epilogue constants, in flight during this layer
       float4 kn[KPL];
-      if (has_next) load_consts(n_conv + 2, kn);
-      // B fragments of one K step: rows of the current tap, chunk of channel step cs
-      int row[2], sw[2], nrow[2], nsw[2];
-      auto rows_for = [&](int tap, int(&rr)[2], int(&ss)[2]) {
+      if (has_next && wn == 0) load_consts(n_conv + 2, kn);
+      // B fragments of one K step.  Channel step cs reads logical chunk
+      // lc = 2 cs + lhi of the tap's row, at chunk position (lc + rot) mod NC with
+      // rot the row's rotation: from a per-tap base b0 = row + 16 (lhi + rot) the
+      // address is b0 + 32 cs, except for the last steps, where lc + rot can pass
+      // the row's end and the base is chosen per lane once per tap.
+      constexpr int WRAP0 = (R::NC - 1 - R::RM) / 2;  // first step that can wrap
+      constexpr int NWRAP = CPT > WRAP0 ? CPT - WRAP0 : 0;
+      struct TapRows {
+        int b0[NBW];
+        int bw[NBW][NWRAP > 0 ? NWRAP : 1];
+      };
+      TapRows row, nrow;
+      auto rows_for = [&](int tap, TapRows& tr) {
         const int dy = tap / 3 - 1, dx = tap % 3 - 1;
 #pragma unroll
-        for (int n = 0; n < 2; ++n) {
-          const int j = n * 32 + l32, r = (j >> 3) + dy, cc = (j & 7) + dx;
+        for (int n = 0; n < NBW; ++n) {
+          const int j = (n0 + n) * 32 + l32, r = (j >> 3) + dy, cc = (j & 7) + dx;
           const bool ok = (unsigned)r < 8u && (unsigned)cc < 8u;
           const int src = r * 8 + cc;
           const int ra = in_off + src * RB, rz = OFF_Z + ((src * RB) & 255);
           const int msk = -(int)ok;
-          rr[n] = (ra & msk) | (rz & ~msk);
-          ss[n] = R::sw(src);
+          const int x = lhi + R::sw(src);
+          tr.b0[n] = ((ra & msk) | (rz & ~msk)) + 16 * x;
+#pragma unroll
+          for (int k = 0; k < NWRAP; ++k)
+            tr.bw[n][k] = tr.b0[n] - (2 * (WRAP0 + k) + x >= R::NC ? 16 * R::NC : 0);
         }
       };
-      auto load_b = [&](const int(&rr)[2], const int(&ss)[2], int cs, frag_t(&dst)[2]) {
-        const int lc = 2 * cs + lhi;
+      auto load_b = [&](const TapRows& tr, auto cs_c, frag_t(&dst)[NBW]) {
+        constexpr int cs = decltype(cs_c)::value;
 #pragma unroll
-        for (int n = 0; n < 2; ++n)
-          dst[n] = *reinterpret_cast<const frag_t*>(smem + rr[n] + (R::pos(lc, ss[n]) << 4));
+        for (int n = 0; n < NBW; ++n) {
+          int base;
+          if constexpr (cs >= WRAP0) base = tr.bw[n][cs - WRAP0];
+          else base = tr.b0[n];
+          dst[n] = *reinterpret_cast<const frag_t*>(smem + base + 32 * cs);
+        }
       };
-      frag_t bc[2], bn[2];
-      rows_for(0, row, sw);
-      load_b(row, sw, 0, bc);
+      frag_t bc[NBW], bn[NBW];
+      rows_for(0, row);
+      load_b(row, std::integral_constant<int, 0>{}, bc);
 
       // one tap: CPT K steps; R0 = ring slot of its first step
       auto tap_body = [&](auto r0_c, auto first_c, int tap) {
         constexpr int R0 = decltype(r0_c)::value;
         constexpr bool FIRST = decltype(first_c)::value;
-        rows_for(tap + 1, nrow, nsw);
+        rows_for(tap + 1, nrow);
         static_for<0, CPT>([&](auto cs_c) {
           constexpr int cs = decltype(cs_c)::value;
           constexpr int cur = (R0 + cs) % NBUF;
@@ -376,33 +424,27 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             // step tap*CPT + cs + NBUF-1 of this layer (of the next layer past its end;
             // past the network's last layer this layer is re-read and never used)
             const int gi = tap * CPT + cs + NBUF - 1;
-            const uint8_t* nxt = wl + (size_t)gi * C::STEP_BYTES;
-            nxt = (has_next || gi < C::S) ? nxt : wl;
-            load_step(A[(cur + NBUF - 1) % NBUF], nxt);
+            load_step(A[(cur + NBUF - 1) % NBUF], wl + ((has_next || gi < C::S) ? gi * C::STEP_BYTES : 0));
           }
-          if constexpr (cs + 1 < CPT) load_b(row, sw, cs + 1, bn);
-          else load_b(nrow, nsw, 0, bn);
+          if constexpr (cs + 1 < CPT) load_b(row, std::integral_constant<int, cs + 1>{}, bn);
+          else load_b(nrow, std::integral_constant<int, 0>{}, bn);
 #pragma unroll
           for (int m = 0; m < DNMB; ++m)
 #pragma unroll
-            for (int n = 0; n < 2; ++n)
+            for (int n = 0; n < NBW; ++n)
               c[m][n] = T::mma(A[cur][m], bc[n], (FIRST && cs == 0) ? acc_t{} : c[m][n]);
 #pragma unroll
-          for (int n = 0; n < 2; ++n) bc[n] = bn[n];
+          for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
           // each MFMA followed by one of the next step's LDS reads, then by one of
           // the prefetched step's weight loads
           static_for<0, DNMB * 2>([&](auto i_c) {
             constexpr int i = decltype(i_c)::value;
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            if constexpr (i < 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if constexpr (i < NBW) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             if constexpr (i < DNMB) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
           });
         });
-#pragma unroll
-        for (int n = 0; n < 2; ++n) {
-          row[n] = nrow[n];
-          sw[n] = nsw[n];
-        }
+        row = nrow;
       };
       constexpr int U = NBUF / gcd_c(CPT, NBUF), NIT = 8 / U, REM = 8 % U;
       tap_body(std::integral_constant<int, LB>{}, std::true_type{}, 0);
@@ -439,8 +481,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             for (int r = 0; r < 4; ++r) {
               const int pc = ch0 + r - DFR;
 #pragma unroll
-              for (int n = 0; n < 2; ++n) {
-                const int sq = 32 * n + l32;
+              for (int n = 0; n < NBW; ++n) {
+                const int sq = 32 * (n0 + n) + l32;
                 pt[pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3)] =
                     med3(__builtin_fmaf((float)c[m][n][4 * q + r], mv[r], bv[r]), 0.0f, cap);
               }
@@ -450,7 +492,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         wave_lds_sync();
         // (2) lane pc < g: board sum (fp64) and maximum of its row; g = [mean, max]
         double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
-        if (lane < DG) {
+        if (wn == 0 && lane < DG) {
           double sum = 0.0;
           float mx = 0.0f;  // activations are >= 0
 #pragma unroll
@@ -500,8 +542,10 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           }
         }
         float* cb = reinterpret_cast<float*>(smem + C::OFF_C);
-        cb[lane] = (float)c0;
-        if (lane + 64 < DFR) cb[lane + 64] = (float)c1;
+        if (wn == 0) {
+          cb[lane] = (float)c0;
+          if (lane + 64 < DFR) cb[lane + 64] = (float)c1;
+        }
         wave_lds_sync();
       }
 
@@ -516,10 +560,10 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
       constexpr bool RHI = !QUANT && SECOND;    // residual hi parts, read in place
       float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
-      uint32_t rcode[RCODE ? EP_RING : 1][2];
-      uint2 rhi[RHI ? EP_RING : 1][2];
+      uint32_t rcode[RCODE ? EP_RING : 1][NBW];
+      uint2 rhi[RHI ? EP_RING : 1][NBW];
       auto ep_addr = [&](int m, int q, int n) {
-        const int j = n * 32 + l32;
+        const int j = (n0 + n) * 32 + l32;
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
         const int rowo = out_off + j * RB;
         if constexpr (QUANT) return rowo + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15);
@@ -533,11 +577,11 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         if constexpr (POOL) kc[slot] = *reinterpret_cast<const float4*>(smem + C::OFF_C + ch0 * 4);
         if constexpr (RCODE) {
 #pragma unroll
-          for (int n = 0; n < 2; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
+          for (int n = 0; n < NBW; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
         }
         if constexpr (RHI) {
 #pragma unroll
-          for (int n = 0; n < 2; ++n) rhi[slot][n] = *reinterpret_cast<const uint2*>(smem + ep_addr(m, q, n));
+          for (int n = 0; n < NBW; ++n) rhi[slot][n] = *reinterpret_cast<const uint2*>(smem + ep_addr(m, q, n));
         }
       };
       static_for<0, EP_AHEAD>([&](auto k_c) { ep_load(k_c); });
@@ -546,7 +590,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
         const float4 bb = kb[slot];
 #pragma unroll
-        for (int n = 0; n < 2; ++n) {
+        for (int n = 0; n < NBW; ++n) {
           const int addr = ep_addr(m, q, n);
           const acc_t& v = c[m][n];
           if constexpr (!QUANT) {
@@ -601,7 +645,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           }
         }
       });
-      if (has_next) store_consts((n_conv + 1) & 1, kn);
+      if (has_next && wn == 0) store_consts((n_conv + 1) & 1, kn);
       __syncthreads();
     };
 
@@ -624,14 +668,17 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       for (int q = 0; q < 4; ++q) {
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
 #pragma unroll
-        for (int n = 0; n < 2; ++n) {
-          const int j = n * 32 + l32;
+        for (int n = 0; n < NBW; ++n) {
+          const int j = (n0 + n) * 32 + l32;
           *reinterpret_cast<uint2*>(smem + C::OFF_X + j * C::RBX + (RX::pos(ch0 >> 3, RX::sw(j)) << 4) + 8 * lhi) =
               make_uint2(rlo[m][n][2 * q], rlo[m][n][2 * q + 1]);
         }
       }
   }
   __syncthreads();
+
+  // the heads run in the first wave; from here on no workgroup barrier
+  if (wn != 0) return;
 
   // ---- embedding: E[row][sq] = sum_f Wemb[row][f] h[f][sq], rows = tokens then value channels
   f32x16 tok[DTB][2];   // token rows (accumulators, then values)
@@ -680,7 +727,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       }
     }
   }
-  __syncthreads();  // H and X are dead from here on
+  wave_sync();  // H and X are dead from here on
 
   // token values relu(acc * scale + bias); value features u[c][sq] to LDS
   const float* HC = reinterpret_cast<const float*>(smem + C::OFF_HC);
@@ -849,7 +896,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       for (int k = 0; k < 4; ++k) O[(l32 - 24) * 4 + k] = Oa[k] * log2e;
     }
   }
-  wave_lds_sync();
+  wave_sync();
 
   // ---- legal-action softmax: lane owns the runs of 4 actions at 256 i + 4 lane
   {
@@ -945,15 +992,3 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
 }  // namespace
 
-hipError_t az_launch_deployed(int dtype, const AzDevNet& n, const float* planes, const uint8_t* legal, int B,
-                              float* policy, float* value, float* wdl, hipStream_t s) {
-  (void)hipGetLastError();
-  if (n.filters != DF || B <= 0) return hipErrorInvalidValue;
-  if (dtype == AZ_INT8)
-    hipLaunchKernelGGL(az_dep_kernel<MK_I8>, dim3(B), dim3(64), 0, s, n, planes, legal, policy, value, wdl);
-  else if (dtype == AZ_BF16)
-    hipLaunchKernelGGL(az_dep_kernel<MK_BF16>, dim3(B), dim3(64), 0, s, n, planes, legal, policy, value, wdl);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
-}

@@ -169,18 +169,32 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // first weight group of the tower, in flight during the stem
   // Weight fragments: a ring of NBUF prefetch groups; group g of a layer lives in
   // buffer g % NBUF and is loaded NBUF - 1 groups before its use.
+  // The stream is read through a buffer resource: the lane's offset is a
+  // constant VGPR and a group's byte offset a scalar, so weight loads cost no
+  // vector address arithmetic in the K loop.
   constexpr int NBUF = C::NBUF;
-  const uint8_t* tw = static_cast<const uint8_t*>(p.tower_w) + (size_t)(mb0 * 64 + lane) * T::FB;
+  const __amdgpu_buffer_rsrc_t twr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.tower_w), (short)0, (int)(2 * p.blocks * C::LAYER_BYTES), 0x00020000);
+  const int tvoff = (mb0 * 64 + lane) * T::FB;
   frag_t A[NBUF][G][MBW];
-  auto load_group = [&](frag_t(&dst)[G][MBW], const uint8_t* src) {
+  auto load_group = [&](frag_t(&dst)[G][MBW], int soff) {
 #pragma unroll
     for (int s = 0; s < G; ++s)
 #pragma unroll
-      for (int m = 0; m < MBW; ++m) dst[s][m] = g_frag<MK>(src + s * C::STEP_BYTES + m * 64 * T::FB);
+      for (int m = 0; m < MBW; ++m) {
+        const int o = soff + s * C::STEP_BYTES + m * 64 * T::FB;
+        if constexpr (T::FB == 16) {
+          dst[s][m] = __builtin_bit_cast(frag_t, __builtin_amdgcn_raw_buffer_load_b128(twr, tvoff, o, 0));
+        } else {
+          const i32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(twr, tvoff, o, 0);
+          const i32x4 hi = __builtin_amdgcn_raw_buffer_load_b128(twr, tvoff, o + 16, 0);
+          dst[s][m] = __builtin_bit_cast(frag_t, i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+        }
+      }
   };
   static_for<0, NBUF - 1>([&](auto i_c) {
     constexpr int i = decltype(i_c)::value;
-    load_group(A[i], tw + (size_t)i * G * C::STEP_BYTES);
+    load_group(A[i], i * G * C::STEP_BYTES);
   });
   // per-layer epilogue constants: thread t < F/2 carries float4 t of [bias | qmul]
   auto load_consts = [&](int k) -> float4 {  // k = 1 + conv index (0 = stem)
@@ -299,7 +313,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     auto conv = [&](auto second_c, auto lb_c, int n_conv) {
       constexpr bool SECOND = decltype(second_c)::value;
       constexpr int LB = decltype(lb_c)::value;  // ring slot of the layer's first group
-      const uint8_t* wl = tw + (size_t)n_conv * C::LAYER_BYTES;
+      const int wl = n_conv * (int)C::LAYER_BYTES;  // byte offset of the layer in the stream
       const bool has_next = n_conv + 1 < nconv;
       const int in_off = SECOND ? OFF_T : OFF_H;
       const int out_off = SECOND ? OFF_H : OFF_T;
@@ -339,9 +353,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             // group tap*GPT + gs + NBUF-1 of this layer, i.e. of the next layer past
             // the end (layers are contiguous)
             const int gi = tap * GPT + gs + NBUF - 1;
-            const uint8_t* nxt = wl + (size_t)gi * G * C::STEP_BYTES;
-            nxt = (has_next || gi < GPL) ? nxt : wl;
-            load_group(A[(cur + NBUF - 1) % NBUF], nxt);
+            load_group(A[(cur + NBUF - 1) % NBUF], wl + ((has_next || gi < GPL) ? gi * G * C::STEP_BYTES : 0));
           }
           if constexpr (cs + 1 < CPT) load_b(row, sw, cs + 1, bn);
           else load_b(nrow, nsw, 0, bn);

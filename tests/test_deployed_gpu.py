@@ -52,7 +52,7 @@ def _scales(shape, blob):
     return OD.weight_scales(shape, blob), np.full(2 * shape.blocks + 1, RELU6_SCALE, np.float32)
 
 
-def gpu_eval(shape, blob, dtype, planes, legal, ws=None, acs=None):
+def gpu_eval(shape, blob, dtype, planes, legal, ws=None, acs=None, tiling=0):
     import torch
 
     import paper_2609_37447_amd as az
@@ -60,6 +60,8 @@ def gpu_eval(shape, blob, dtype, planes, legal, ws=None, acs=None):
     net = az.az_net_load(az.spec_from_shape(shape, B), blob, dtype, ws, acs)
     try:
         assert az.az_net_moves(net) == 1880
+        if tiling:
+            az.az_net_set_tiling(net, tiling)
         dev = torch.device("cuda:0")
         pl = torch.from_numpy(np.ascontiguousarray(planes, dtype=np.float32)).to(dev)
         lg = torch.from_numpy(np.ascontiguousarray(legal, dtype=np.uint8)).to(dev)
@@ -169,3 +171,24 @@ def test_deployed_rows_do_not_depend_on_the_batch():
     one = gpu_eval(shape, blob, "int8", planes[5:6], legal[5:6], ws, acs)
     for a, b in zip(full, one):
         assert np.array_equal(a[5:6], b)
+
+
+@pytest.mark.parametrize("dtype", ["int8", "bf16"])
+def test_deployed_tilings_agree_bitwise(dtype):
+    # one and two waves per board take every sum in the same order
+    import paper_2609_37447_amd as az
+    shape = _shape(4)
+    blob = azgen.make_weights(shape, 1036, alpha_fold=True, bf16=True)
+    planes, legal = _inputs(shape, 21, 2236)
+    legal = _edge_rows(legal)
+    ws, acs = _scales(shape, blob) if dtype == "int8" else (None, None)
+    one = gpu_eval(shape, blob, dtype, planes, legal, ws, acs, tiling=1)
+    two = gpu_eval(shape, blob, dtype, planes, legal, ws, acs, tiling=2)
+    for a, b in zip(one, two):
+        assert np.array_equal(a, b)
+    net = az.az_net_load(az.spec_from_shape(shape, 512), blob, dtype, ws, acs)
+    try:
+        assert az.az_net_tiling_for(net, 64) == 2 and az.az_net_tiling_for(net, 512) == 1
+        assert az.az_net_set_tiling(net, 3, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
+    finally:
+        az.az_net_free(net)
