@@ -49,10 +49,10 @@ def kernel_source(shape):
 # for the kernel source it was taken on only: any other source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {  # (workload, tiling): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    ("net20x128_int8_b1024", 3): ("94a0de94aaa0eef2e0bcb9398aa55cff0e38e3f2fc36dc854802da5a70803d0a",
-                                  32044.8, 18704.0),
-    ("deployed14x160_int8_b1024", 0): ("980e03fbb97b6b5e7c09f0387c587ef848c594f80146bd7ee44554172088b0c2",
-                                       45325.1, 24704.0),
+    ("net20x128_int8_b1024", 3): ("faf2c3970238b8113f568cabf1e9363b742d350fdec26bd0ffc19cbf57c667f6",
+                                  33413.4, 18704.0),
+    ("deployed14x160_int8_b1024", 0): ("24082077b51b53ce5cef9da3fc21122d80028dd2839eb0235160b812ec79a625",
+                                       46261.5, 30204.2),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.

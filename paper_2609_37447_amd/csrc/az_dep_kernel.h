@@ -4,14 +4,11 @@
 // outputs", Section 4.3 "Convolution, attention, and global context", "Three
 // policy representations", "Value and training-only heads", Appendix D).
 //
-// One workgroup evaluates one board end to end.  With one wave per board (the
-// default from ~a quarter of the chip's boards up), four such workgroups share a
-// compute unit (int8), one per SIMD, and the wave owns every output tile: five
-// 32-channel MFMA blocks times both half-board square blocks, so global pooling,
-// the heads and both softmaxes need no exchange with other waves.  For small
-// batches, whose boards do not fill the chip, two waves share a board: each owns
-// one half-board square block of every layer, the pooled statistics meet in
-// LDS, and the heads run in the first wave.
+// One workgroup is one wave and evaluates one board end to end; four such
+// workgroups share a compute unit (int8), one per SIMD.  The wave owns every
+// output channel (five 32-channel MFMA blocks) and both half-board square
+// blocks of every layer, so global pooling, the heads and both softmaxes need
+// no exchange with other waves.
 //
 // Tower.  Every 3x3 convolution is an implicit GEMM D[ch][sq] = sum_k
 // W[ch][k] X[k][sq], k = tap * C + c, with weights as the A operand (streamed
@@ -150,12 +147,8 @@ struct DepCfg {
   static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
 };
 
-// NWB waves per board (one workgroup per board): 1 (every output tile of the
-// board in one wave; four boards per compute unit) or 2 (the two half-board
-// square blocks in two waves, for small batches whose boards do not fill the
-// chip; the heads then run in the first wave).
-template <int MK, int NWB>
-__global__ __attribute__((amdgpu_flat_work_group_size(64 * NWB, 64 * NWB), amdgpu_waves_per_eu(1, 1))) void
+template <int MK>
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 64), amdgpu_waves_per_eu(1, 1))) void
 az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal,
               float* __restrict__ policy, float* __restrict__ value, float* __restrict__ wdl) {
   using C = DepCfg<MK>;
@@ -168,12 +161,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[C::SMEM];
 
-  static_assert(NWB == 1 || NWB == 2, "waves per board");
-  constexpr int NBW = 2 / NWB;  // half-board square blocks per wave
-  constexpr int NT = 64 * NWB;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wn = NWB == 1 ? 0 : __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n0 = wn * NBW;      // the wave's first square block
+  constexpr int NBW = 2;  // half-board square blocks (the wave owns the whole board)
+  const int lane = threadIdx.x;
   const int l32 = lane & 31, lhi = lane >> 5;
   const int b = blockIdx.x;
   const int Cin = p.in_planes;
@@ -185,26 +174,26 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   uint32_t rlo[QUANT ? 1 : DNMB][QUANT ? 1 : NBW][QUANT ? 1 : 8];
 
   // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
-  for (int i = tid; i < C::ZB / 16; i += NT)
+  for (int i = lane; i < C::ZB / 16; i += 64)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
-  for (int i = tid; i < DF; i += NT) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
+  for (int i = lane; i < DF; i += 64) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
   {
-    // item k = planes 8k..8k+7 (wave wn takes k = wn, wn + NWB, ...): lane =
-    // square, eight coalesced loads, one 16-byte store
-    constexpr int KI = DCP / 8 / NWB;
+    // item k = planes 8k..8k+7: lane = square, eight coalesced loads, one
+    // 16-byte store
+    constexpr int KI = DCP / 8;
     float pv[KI][8];
 #pragma unroll
     for (int ki = 0; ki < KI; ++ki)
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
-        const int c = 8 * (wn + NWB * ki) + t;
+        const int c = 8 * ki + t;
         const bool ok = c < Cin;
         const float x = planes[((size_t)b * Cin + (ok ? c : 0)) * 64 + lane];
         pv[ki][t] = ok ? x : 0.0f;
       }
 #pragma unroll
     for (int ki = 0; ki < KI; ++ki) {
-      const int k = wn + NWB * ki;
+      const int k = ki;
       *reinterpret_cast<uint4*>(smem + OFF_T + lane * 128 + ((k ^ swz128(lane)) << 4)) =
           make_uint4(pack_bf16x2(pv[ki][0], pv[ki][1]), pack_bf16x2(pv[ki][2], pv[ki][3]),
                      pack_bf16x2(pv[ki][4], pv[ki][5]), pack_bf16x2(pv[ki][6], pv[ki][7]));
@@ -242,7 +231,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       dst[t] = i < KV ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  auto store_consts = [&](int slot, const float4(&v)[KPL]) {  // by the first wave
+  auto store_consts = [&](int slot, const float4(&v)[KPL]) {
     float4* dst = reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT);
 #pragma unroll
     for (int t = 0; t < KPL; ++t)
@@ -251,16 +240,16 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // head constants, staged once: embedding row scale and bias, query and key biases
   {
     float* hc = reinterpret_cast<float*>(smem + C::OFF_HC);
-    for (int i = tid; i < AZ_DEP_EMB_ROWS; i += NT) {
+    for (int i = lane; i < AZ_DEP_EMB_ROWS; i += 64) {
       hc[i] = p.emb_sc[i];
       hc[AZ_DEP_EMB_ROWS + i] = p.emb_bc[i];
     }
-    for (int i = tid; i < DD; i += NT) {
+    for (int i = lane; i < DD; i += 64) {
       hc[2 * AZ_DEP_EMB_ROWS + i] = p.q_b[i];
       hc[2 * AZ_DEP_EMB_ROWS + DD + i] = p.k_b[i];
     }
   }
-  if (wn == 0) {
+  {
     float4 k0[KPL];
     load_consts(1, k0);
     store_consts(0, k0);
@@ -284,7 +273,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       const int tap = st / 4, cs = st % 4, dy = tap / 3 - 1, dx = tap % 3 - 1;
 #pragma unroll
       for (int n = 0; n < NBW; ++n) {
-        const int j = (n0 + n) * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
+        const int j = n * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
         const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
         const int src = r * 8 + c;
         const int row = ok ? OFF_T + src * 128 : OFF_Z + ((src * 128) & 255);
@@ -323,7 +312,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
-          const int j = (n0 + n) * 32 + l32;
+          const int j = n * 32 + l32;
           const f32x16& v = sacc[m][n];
           if constexpr (!QUANT) {
             const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
@@ -369,7 +358,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
       // the next layer's epilogue constants, in flight during this layer
       float4 kn[KPL];
-      if (has_next && wn == 0) load_consts(n_conv + 2, kn);
+      if (has_next) load_consts(n_conv + 2, kn);
       // B fragments of one K step.  Channel step cs reads logical chunk
       // lc = 2 cs + lhi of the tap's row, at chunk position (lc + rot) mod NC with
       // rot the row's rotation: from a per-tap base b0 = row + 16 (lhi + rot) the
@@ -386,7 +375,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         const int dy = tap / 3 - 1, dx = tap % 3 - 1;
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
-          const int j = (n0 + n) * 32 + l32, r = (j >> 3) + dy, cc = (j & 7) + dx;
+          const int j = n * 32 + l32, r = (j >> 3) + dy, cc = (j & 7) + dx;
           const bool ok = (unsigned)r < 8u && (unsigned)cc < 8u;
           const int src = r * 8 + cc;
           const int ra = in_off + src * RB, rz = OFF_Z + ((src * RB) & 255);
@@ -482,7 +471,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
               const int pc = ch0 + r - DFR;
 #pragma unroll
               for (int n = 0; n < NBW; ++n) {
-                const int sq = 32 * (n0 + n) + l32;
+                const int sq = 32 * n + l32;
                 pt[pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3)] =
                     med3(__builtin_fmaf((float)c[m][n][4 * q + r], mv[r], bv[r]), 0.0f, cap);
               }
@@ -492,7 +481,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         wave_lds_sync();
         // (2) lane pc < g: board sum (fp64) and maximum of its row; g = [mean, max]
         double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
-        if (wn == 0 && lane < DG) {
+        if (lane < DG) {
           double sum = 0.0;
           float mx = 0.0f;  // activations are >= 0
 #pragma unroll
@@ -542,10 +531,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           }
         }
         float* cb = reinterpret_cast<float*>(smem + C::OFF_C);
-        if (wn == 0) {
-          cb[lane] = (float)c0;
-          if (lane + 64 < DFR) cb[lane + 64] = (float)c1;
-        }
+        cb[lane] = (float)c0;
+        if (lane + 64 < DFR) cb[lane + 64] = (float)c1;
         wave_lds_sync();
       }
 
@@ -563,7 +550,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       uint32_t rcode[RCODE ? EP_RING : 1][NBW];
       uint2 rhi[RHI ? EP_RING : 1][NBW];
       auto ep_addr = [&](int m, int q, int n) {
-        const int j = (n0 + n) * 32 + l32;
+        const int j = n * 32 + l32;
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
         const int rowo = out_off + j * RB;
         if constexpr (QUANT) return rowo + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15);
@@ -645,7 +632,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           }
         }
       });
-      if (has_next && wn == 0) store_consts((n_conv + 1) & 1, kn);
+      if (has_next) store_consts((n_conv + 1) & 1, kn);
       __syncthreads();
     };
 
@@ -669,16 +656,13 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
-          const int j = (n0 + n) * 32 + l32;
+          const int j = n * 32 + l32;
           *reinterpret_cast<uint2*>(smem + C::OFF_X + j * C::RBX + (RX::pos(ch0 >> 3, RX::sw(j)) << 4) + 8 * lhi) =
               make_uint2(rlo[m][n][2 * q], rlo[m][n][2 * q + 1]);
         }
       }
   }
   __syncthreads();
-
-  // the heads run in the first wave; from here on no workgroup barrier
-  if (wn != 0) return;
 
   // ---- embedding: E[row][sq] = sum_f Wemb[row][f] h[f][sq], rows = tokens then value channels
   f32x16 tok[DTB][2];   // token rows (accumulators, then values)

@@ -490,7 +490,6 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
   // ---- heads: 1x1 convs F -> (P policy planes + 1 value row) as one bf16 GEMM
   const int P = p.policy_planes;
-  const int LB = (P + 1) * 64;
   const int NMV = P * 64;
   // Softmax and value: WPB waves per board.  The board's cells form groups g of
   // 1024; in group g lane l owns the four runs of 4 cells at g*1024 + u*256 + 4l

@@ -346,13 +346,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // for bf16 and fp8, and the two-board medium tiling (two workgroups per compute
 // unit) ties with it for int8.
 int choose_tiling(const az_net* n, int B) {
-  if (n->dtype == AZ_F32) return 0;
-  if (is_deployed(n->spec)) {
-    // deployed network: one wave per board fills the chip from ~1,024 boards
-    // (four per compute unit); below that two waves per board halve the latency
-    if (n->tiling) return n->tiling;
-    return B <= AZ_DEP_TWO_WAVE_MAX_B ? 2 : 1;
-  }
+  if (n->dtype == AZ_F32 || is_deployed(n->spec)) return 0;
   if (n->tiling) return n->tiling;
   const int F = n->spec.filters;
   if (B < 512) return 2;
@@ -678,8 +672,8 @@ int az_eval_batch_wdl(az_net* net, const float* planes, const uint8_t* legal, in
   if (cur != net->device && (e = hipSetDevice(net->device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dep)
-    e = (net->dtype == AZ_INT8 ? az_launch_deployed_int8 : az_launch_deployed_bf16)(
-        choose_tiling(net, B), net->dn, planes, legal, B, policy, value, wdl, s);
+    e = (net->dtype == AZ_INT8 ? az_launch_deployed_int8 : az_launch_deployed_bf16)(net->dn, planes, legal, B,
+                                                                                     policy, value, wdl, s);
   else if (net->dtype == AZ_F32)
     e = az_launch_f32(net->dn, planes, legal, B, policy, value, s);
   else
@@ -701,9 +695,9 @@ int az_net_moves(const az_net* net) {
 
 int az_net_set_tiling(az_net* net, int32_t tiling) {
   if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
-  const bool valid = net->dtype == AZ_F32 ? tiling == 0
-                     : is_deployed(net->spec) ? (tiling >= 0 && tiling <= 2)
-                                              : (tiling == 0 || az_mfma_tiling_valid(net->spec.filters, tiling));
+  const bool valid = (net->dtype == AZ_F32 || is_deployed(net->spec))
+                         ? tiling == 0
+                         : (tiling == 0 || az_mfma_tiling_valid(net->spec.filters, tiling));
   if (!valid)
     return fail(AZ_ERR_INVALID_ARG, "tiling %d not available for this dtype", tiling);
   net->tiling = tiling;
