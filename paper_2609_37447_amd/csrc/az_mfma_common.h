@@ -123,7 +123,7 @@ __device__ __forceinline__ uint32_t pack_codes(float z0, float z1, float z2, flo
 // for int8; fp8 codes are decoded by the hardware conversion).
 template <int MK, int R>
 __device__ __forceinline__ float code_value(uint32_t x) {
-  if constexpr (MK == MK_I8) return (float)(int)(int8_t)(x >> (8 * R));
+  if constexpr (MK == MK_I8) return (float)((x >> (8 * R)) & 0xffu);  // codes are 0..127
   else return __builtin_amdgcn_cvt_f32_fp8((int)x, R);
 }
 
