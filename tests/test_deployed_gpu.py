@@ -183,3 +183,47 @@ def test_deployed_has_a_single_tiling():
             assert az.az_net_set_tiling(net, t, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
     finally:
         az.az_net_free(net)
+
+
+def test_deployed_validate_gate():
+    # deployment validation (top-1 legal agreement, legal-policy KL, value error)
+    # of the int8 deployed network against its bf16 source over the 1,880 actions:
+    # the faithful network passes, one with activation scales x 0.1 does not
+    import torch
+
+    import paper_2609_37447_amd as az
+    from oracle import az_oracle as O
+    shape = _shape(4)
+    blob = azgen.make_weights(shape, 1046, alpha_fold=True, bf16=True)
+    planes, legal = _inputs(shape, 64, 2246)
+    legal = _edge_rows(legal)
+    ws, acs = _scales(shape, blob)
+    dev = torch.device("cuda:0")
+    pl = torch.from_numpy(planes).to(dev)
+    lg = torch.from_numpy(legal).to(dev)
+    spec = az.spec_from_shape(shape, 64)
+    ref = az.az_net_load(spec, blob, "bf16")
+    good = az.az_net_load(spec, blob, "int8", ws, acs)
+    broken = az.az_net_load(spec, blob, "int8", ws, acs * np.float32(0.1))
+    try:
+        r_good = az.validate(good, ref, pl, lg)
+        r_bad = az.validate(broken, ref, pl, lg)
+        print(f"faithful: top1 {r_good['top1']:.3f} KL {r_good['kl']:.4f} |dV| {r_good['dv_max']:.3f}; "
+              f"broken: top1 {r_bad['top1']:.3f} KL {r_bad['kl']:.4f} |dV| {r_bad['dv_max']:.3f}")
+        assert r_good["passed"] and not r_bad["passed"]
+        # per-row metrics against the definition on the same evaluations
+        P = {}
+        for key, net in (("ref", ref), ("test", good)):
+            pol = torch.empty((64, 1880), device=dev)
+            val = torch.empty((64,), device=dev)
+            az.eval_tensors(net, pl, lg, pol, val)
+            P[key] = (pol.cpu().numpy(), val.cpu().numpy())
+        torch.cuda.synchronize()
+        top1, kl, dv = O.compare_outputs(P["ref"][0], P["ref"][1], P["test"][0], P["test"][1], legal)
+        g = r_good["rows"]
+        assert np.array_equal(g[:, 0], top1)
+        assert np.all(np.abs(g[:, 1] - kl) <= 1e-5 + 1e-4 * np.abs(kl))
+        assert np.all(np.abs(g[:, 2] - dv) <= 1e-7)
+    finally:
+        for n in (ref, good, broken):
+            az.az_net_free(n)
