@@ -224,13 +224,15 @@ int az_net_moves(const az_net* net);
  * (default); 1 (large): four boards per workgroup (F = 64, 128) or two
  * (F = 256), one workgroup per compute unit; 2 (small): one board per
  * workgroup; 3 (medium, F = 64 and 128 only): two boards per workgroup, two
- * workgroups per compute unit.  Every tiling computes bitwise the same
- * results.  AZ_F32 and the deployed network have a single tiling and accept
- * only 0.  Returns AZ_OK or AZ_ERR_INVALID_ARG. */
+ * workgroups per compute unit.  The deployed network has two: 1, one wave per
+ * board (several boards per compute unit); 2, four waves per board (one board
+ * per compute unit, for small batches).  Every tiling computes bitwise the
+ * same results.  AZ_F32 has a single tiling and accepts only 0.  Returns
+ * AZ_OK or AZ_ERR_INVALID_ARG. */
 int az_net_set_tiling(az_net* net, int32_t tiling);
 
 /* The tiling az_eval_batch would use for a batch of B (1, 2 or 3; 0 for
- * AZ_F32 and the deployed network), or a negative status. */
+ * AZ_F32), or a negative status. */
 int az_net_tiling_for(const az_net* net, int32_t B);
 
 /* Device bytes held by the handle (packed weights and per-layer constants). */

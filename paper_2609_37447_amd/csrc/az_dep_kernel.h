@@ -4,11 +4,15 @@
 // outputs", Section 4.3 "Convolution, attention, and global context", "Three
 // policy representations", "Value and training-only heads", Appendix D).
 //
-// One workgroup is one wave and evaluates one board end to end; four such
-// workgroups share a compute unit (int8), one per SIMD.  The wave owns every
-// output channel (five 32-channel MFMA blocks) and both half-board square
-// blocks of every layer, so global pooling, the heads and both softmaxes need
-// no exchange with other waves.
+// One workgroup evaluates one board end to end, in one of two tilings.
+// az_dep_kernel (large batches): one wave per workgroup, four such workgroups
+// per compute unit for int8 (one per SIMD); the wave owns every output channel
+// (five 32-channel MFMA blocks) and both half-board square blocks of every
+// layer, so global pooling, the heads and both softmaxes need no exchange with
+// other waves.  az_dep_kernel4 (small batches, where the batch offers about a
+// board per compute unit): four waves, one per SIMD, share a layer's ten 32x32
+// tiles, three at most per SIMD, and meet at a barrier per layer; the heads
+// run in one of them.
 //
 // Tower.  Every 3x3 convolution is an implicit GEMM D[ch][sq] = sum_k
 // W[ch][k] X[k][sq], k = tap * C + c, with weights as the A operand (streamed
@@ -146,6 +150,332 @@ struct DepCfg {
   static constexpr int STEP_BYTES = DNMB * 64 * T::FB;
   static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
 };
+
+
+// Heads of one board, run by one wave (lane = 0..63) once the final tower
+// output h is in LDS (int8: codes in H; bf16: hi parts in H, lo parts in X):
+// embedding, tokens, query-key logits and promotion offsets, legal-action
+// softmax, WDL value head.
+template <int MK>
+__device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, const uint8_t* __restrict__ legal,
+                                          float* __restrict__ policy, float* __restrict__ value,
+                                          float* __restrict__ wdl, int b, int lane) {
+  using C = DepCfg<MK>;
+  using R = Rot<C::RB>;
+  using RX = Rot<C::RBX>;
+  constexpr bool QUANT = C::QUANT;
+  constexpr int RB = C::RB, OFF_H = C::OFF_H;
+  const int l32 = lane & 31, lhi = lane >> 5;
+
+  // ---- embedding: E[row][sq] = sum_f Wemb[row][f] h[f][sq], rows = tokens then value channels
+  f32x16 tok[DTB][2];   // token rows (accumulators, then values)
+  f32x16 uacc[2];       // value rows 128..159
+  {
+    const uint8_t* ew = static_cast<const uint8_t*>(p.emb_w) + (size_t)lane * 16;
+    // A fragments of K step s in ring slot s % 4, loaded three steps ahead
+    constexpr int ES = DF / 16, ER = 4;
+    bf16x8 awr[ER][DEMB];
+    auto load_e = [&](int st) {
+#pragma unroll
+      for (int m = 0; m < DEMB; ++m) awr[st % ER][m] = g_frag<MK_BF16>(ew + (st * DEMB + m) * 64 * 16);
+    };
+#pragma unroll
+    for (int st = 0; st < ER - 1; ++st) load_e(st);
+#pragma unroll
+    for (int s = 0; s < ES; ++s) {
+      if (s + ER - 1 < ES) load_e(s + ER - 1);
+      const bf16x8(&aw)[DEMB] = awr[s % ER];
+      bf16x8 bx[2], bh[2];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int j = n * 32 + l32;
+        if constexpr (QUANT) {
+          // eight codes of channels 16 s + 8 lhi .. + 7, exact in bf16
+          const uint2 v = *reinterpret_cast<const uint2*>(smem + OFF_H + j * RB + (R::pos(s, R::sw(j)) << 4) + 8 * lhi);
+          bx[n] = __builtin_bit_cast(
+              bf16x8, make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
+                                 pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
+                                 pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
+                                 pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y))));
+        } else {
+          bx[n] = *reinterpret_cast<const bf16x8*>(smem + C::OFF_X + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+          bh[n] = *reinterpret_cast<const bf16x8*>(smem + OFF_H + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+        }
+      }
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+#pragma unroll
+        for (int m = 0; m < DTB; ++m) {
+          tok[m][n] = mma_bf16(aw[m], bx[n], s == 0 ? f32x16{} : tok[m][n]);
+          if constexpr (!QUANT) tok[m][n] = mma_bf16(aw[m], bh[n], tok[m][n]);
+        }
+        uacc[n] = mma_bf16(aw[DTB], bx[n], s == 0 ? f32x16{} : uacc[n]);
+        if constexpr (!QUANT) uacc[n] = mma_bf16(aw[DTB], bh[n], uacc[n]);
+      }
+    }
+  }
+  wave_sync();  // H and X are dead from here on
+
+  // token values relu(acc * scale + bias); value features u[c][sq] to LDS
+  const float* HC = reinterpret_cast<const float*>(smem + C::OFF_HC);
+  {
+#pragma unroll
+    for (int m = 0; m < DTB; ++m)
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int r0 = 32 * m + 8 * jq + 4 * lhi;
+        const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+        const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
+        const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tok[m][n][4 * jq + r] = fmaxf(__builtin_fmaf(tok[m][n][4 * jq + r], sv[r], bv[r]), 0.0f);
+      }
+    float* U = reinterpret_cast<float*>(smem + C::OFF_U);
+    const int V = p.value_channels;
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      const int r0 = DD + 8 * jq + 4 * lhi;
+      const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+      const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
+      const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ch = 8 * jq + 4 * lhi + r;
+        if (ch < V) {
+#pragma unroll
+          for (int n = 0; n < 2; ++n) {
+            float u = __builtin_fmaf(uacc[n][4 * jq + r], sv[r], bv[r]);
+            if (p.value_conv_relu) u = fmaxf(u, 0.0f);
+            U[ch * 64 + n * 32 + l32] = u;
+          }
+        }
+      }
+    }
+  }
+
+  // Operand fragments from accumulators: K step s of a 128-row accumulator
+  // set X[4][2] (rows = the product's K dimension) for column block n holds
+  // positions 8s .. 8s+7 of the lane's 64 accumulator values.
+  auto frags_of = [&](const f32x16(&X)[DTB][2], int n, int s, bf16x8& hi, bf16x8& lo) {
+    float x[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) x[t] = X[(8 * s + t) / 16][n][(8 * s + t) % 16];
+    split8(x, hi, lo);
+  };
+  // Q^T = Wq tok^T + bq and K^T = Wk tok^T + bk in one pass over the token
+  // fragments (split operands); rows of Q^T and K^T in the token accumulators'
+  // register order, so the token values die as the pass ends
+  f32x16 Qa[DTB][2], Ka[DTB][2];
+  {
+    const uint8_t* qp = static_cast<const uint8_t*>(p.q_w) + (size_t)lane * 16;
+    const uint8_t* kp = static_cast<const uint8_t*>(p.k_w) + (size_t)lane * 16;
+    // A fragments of K step s in ring slot s % 2, loaded one step ahead
+    constexpr int QS = DD / 16, QR = 2;
+    bf16x8 aqr[QR][DTB], akr[QR][DTB];
+    auto load_qk = [&](int st) {
+#pragma unroll
+      for (int m = 0; m < DTB; ++m) {
+        aqr[st % QR][m] = g_frag<MK_BF16>(qp + (st * DTB + m) * 64 * 16);
+        akr[st % QR][m] = g_frag<MK_BF16>(kp + (st * DTB + m) * 64 * 16);
+      }
+    };
+#pragma unroll
+    for (int st = 0; st < QR - 1; ++st) load_qk(st);
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+      if (s + QR - 1 < QS) load_qk(s + QR - 1);
+      const bf16x8(&aq)[DTB] = aqr[s % QR];
+      const bf16x8(&ak)[DTB] = akr[s % QR];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        bf16x8 xh, xl;
+        frags_of(tok, n, s, xh, xl);
+#pragma unroll
+        for (int m = 0; m < DTB; ++m) {
+          Qa[m][n] = mma_bf16(aq[m], xh, s == 0 ? f32x16{} : Qa[m][n]);
+          Qa[m][n] = mma_bf16(aq[m], xl, Qa[m][n]);
+          Ka[m][n] = mma_bf16(ak[m], xh, s == 0 ? f32x16{} : Ka[m][n]);
+          Ka[m][n] = mma_bf16(ak[m], xl, Ka[m][n]);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < DTB; ++m)
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int r0 = 32 * m + 8 * jq + 4 * lhi;
+        const float4 bq = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + r0);
+        const float4 bk = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + DD + r0);
+        const float qv[4] = {bq.x, bq.y, bq.z, bq.w}, kv[4] = {bk.x, bk.y, bk.z, bk.w};
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            Qa[m][n][4 * jq + r] += qv[r];
+            Ka[m][n][4 * jq + r] += kv[r];
+          }
+      }
+  }
+
+  // S[f][t] = sum_d Q[f][d] K[t][d] (hi*hi + hi*lo + lo*hi) and the promotion
+  // offsets O^T[k][t] = sum_d Wp[k][d] K[t][d] for the last row's destinations
+  // action table entries and legal-mask words of the softmax, in flight
+  // during the query-key products
+  constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
+  uint4 tbl[NIT];
+  uint32_t mkw[NIT];
+  {
+    const uint8_t* lg = legal + (size_t)b * NA;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      const bool in = a0 < NA;
+      tbl[i] = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
+      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
+      mkw[i] = in ? mk0 : 0u;
+    }
+  }
+  f32x16 Sa[2][2], Oa;
+  {
+    const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
+    bf16x8 apw[DD / 16];  // every K step's promotion-weight fragment, loaded up front
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) apw[s] = g_frag<MK_BF16>(pw + s * 64 * 16);
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) {
+      bf16x8 qh[2], ql[2], kh[2], kl[2];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        frags_of(Qa, n, s, qh[n], ql[n]);
+        frags_of(Ka, n, s, kh[n], kl[n]);
+      }
+#pragma unroll
+      for (int mf = 0; mf < 2; ++mf)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          Sa[mf][nt] = mma_bf16(qh[mf], kh[nt], s == 0 ? f32x16{} : Sa[mf][nt]);
+          Sa[mf][nt] = mma_bf16(qh[mf], kl[nt], Sa[mf][nt]);
+          Sa[mf][nt] = mma_bf16(ql[mf], kh[nt], Sa[mf][nt]);
+        }
+      Oa = mma_bf16(apw[s], kh[1], s == 0 ? f32x16{} : Oa);
+      Oa = mma_bf16(apw[s], kl[1], Oa);
+    }
+  }
+  // logits pre-scaled by log2(e) for the exp2 softmax
+  {
+    const float log2e = 1.4426950408889634f;
+    const float ss = log2e / sqrtf((float)DD);
+    float* S = reinterpret_cast<float*>(smem + C::OFF_S);
+#pragma unroll
+    for (int mf = 0; mf < 2; ++mf)
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int f = 32 * mf + 8 * (v / 4) + 4 * lhi + v % 4, t = 32 * nt + l32;
+          S[f * 64 + t] = Sa[mf][nt][v] * ss;
+        }
+    float* O = reinterpret_cast<float*>(smem + C::OFF_O);
+    if (lhi == 0 && l32 >= 24) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) O[(l32 - 24) * 4 + k] = Oa[k] * log2e;
+    }
+  }
+  wave_sync();
+
+  // ---- legal-action softmax: lane owns the runs of 4 actions at 256 i + 4 lane
+  {
+    const float* S = reinterpret_cast<const float*>(smem + C::OFF_S);
+    const float* O = reinterpret_cast<const float*>(smem + C::OFF_O);
+    float e[NIT][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      const bool in = a0 < NA;  // NA is a multiple of 4
+      const uint4 tb = tbl[i];
+      const uint32_t mk = mkw[i];
+      const uint32_t te[4] = {tb.x, tb.y, tb.z, tb.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t x = te[r], pr = x >> 12;
+        const float z = S[x & 4095u] + (pr ? O[pr - 1] : 0.0f);
+        const bool ok = in && ((mk >> (8 * r)) & 0xffu);
+        e[i][r] = ok ? z : -INFINITY;
+        mx = fmaxf(mx, e[i][r]);
+      }
+    }
+    mx = wave_max(mx);
+    const float msub = mx == -INFINITY ? 0.0f : mx;
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        e[i][r] = __builtin_amdgcn_exp2f(e[i][r] - msub);  // exp2(-inf) = 0
+        sum += e[i][r];
+      }
+    sum = wave_sum(sum);
+    const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
+    float* pol = policy + (size_t)b * NA;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      if (a0 < NA)
+        *reinterpret_cast<float4*>(pol + a0) = make_float4(e[i][0] * inv, e[i][1] * inv, e[i][2] * inv, e[i][3] * inv);
+    }
+  }
+
+  // ---- WDL head: y = relu(W1 u + b1), z = W2 y + b2, softmax, value = W - L
+  {
+    const float* U = reinterpret_cast<const float*>(smem + C::OFF_U);
+    const int H = p.value_hidden, NU = p.value_channels * 64;
+    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
+    for (int k0 = 0; k0 < H; k0 += 64) {
+      const int k = k0 + lane;
+      const bool ok = k < H;
+      const int kk = ok ? k : 0;
+      float y = p.wdl_fc1_b[kk];
+      // fc1 row of unit kk in chunks of 16 inputs, the next chunk in flight
+      // (NU is a multiple of 64)
+      float wa[16], wb[16];
+      auto ld = [&](float(&d)[16], int i0) {
+#pragma unroll
+        for (int t = 0; t < 16; ++t) d[t] = p.wdl_fc1_t[(size_t)(i0 + t) * H + kk];
+      };
+      ld(wa, 0);
+      for (int i0 = 0; i0 < NU; i0 += 32) {
+        ld(wb, i0 + 16);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wa[t], U[i0 + t], y);
+        if (i0 + 32 < NU) ld(wa, i0 + 32);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wb[t], U[i0 + 16 + t], y);
+      }
+      y = ok ? fmaxf(y, 0.0f) : 0.0f;
+      z0 = __builtin_fmaf(p.wdl_fc2_w[kk], y, z0);
+      z1 = __builtin_fmaf(p.wdl_fc2_w[H + kk], y, z1);
+      z2 = __builtin_fmaf(p.wdl_fc2_w[2 * H + kk], y, z2);
+    }
+    z0 = wave_sum(z0) + p.wdl_fc2_b[0];
+    z1 = wave_sum(z1) + p.wdl_fc2_b[1];
+    z2 = wave_sum(z2) + p.wdl_fc2_b[2];
+    const float m = fmaxf(z0, fmaxf(z1, z2));
+    const float e0 = expf(z0 - m), e1 = expf(z1 - m), e2 = expf(z2 - m);
+    const float is = 1.0f / (e0 + e1 + e2);
+    if (lane == 0) {
+      const float pw = e0 * is, pd = e1 * is, pl = e2 * is;
+      value[b] = pw - pl;
+      if (wdl) {
+        wdl[3 * (size_t)b + 0] = pw;
+        wdl[3 * (size_t)b + 1] = pd;
+        wdl[3 * (size_t)b + 2] = pl;
+      }
+    }
+  }
+}
 
 template <int MK>
 __global__ __attribute__((amdgpu_flat_work_group_size(64, 64), amdgpu_waves_per_eu(1, 1))) void
@@ -664,315 +994,556 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   }
   __syncthreads();
 
-  // ---- embedding: E[row][sq] = sum_f Wemb[row][f] h[f][sq], rows = tokens then value channels
-  f32x16 tok[DTB][2];   // token rows (accumulators, then values)
-  f32x16 uacc[2];       // value rows 128..159
-  {
-    const uint8_t* ew = static_cast<const uint8_t*>(p.emb_w) + (size_t)lane * 16;
-    // A fragments of K step s in ring slot s % 4, loaded three steps ahead
-    constexpr int ES = DF / 16, ER = 4;
-    bf16x8 awr[ER][DEMB];
-    auto load_e = [&](int st) {
-#pragma unroll
-      for (int m = 0; m < DEMB; ++m) awr[st % ER][m] = g_frag<MK_BF16>(ew + (st * DEMB + m) * 64 * 16);
-    };
-#pragma unroll
-    for (int st = 0; st < ER - 1; ++st) load_e(st);
-#pragma unroll
-    for (int s = 0; s < ES; ++s) {
-      if (s + ER - 1 < ES) load_e(s + ER - 1);
-      const bf16x8(&aw)[DEMB] = awr[s % ER];
-      bf16x8 bx[2], bh[2];
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        const int j = n * 32 + l32;
-        if constexpr (QUANT) {
-          // eight codes of channels 16 s + 8 lhi .. + 7, exact in bf16
-          const uint2 v = *reinterpret_cast<const uint2*>(smem + OFF_H + j * RB + (R::pos(s, R::sw(j)) << 4) + 8 * lhi);
-          bx[n] = __builtin_bit_cast(
-              bf16x8, make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
-                                 pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
-                                 pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
-                                 pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y))));
-        } else {
-          bx[n] = *reinterpret_cast<const bf16x8*>(smem + C::OFF_X + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
-          bh[n] = *reinterpret_cast<const bf16x8*>(smem + OFF_H + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
-        }
-      }
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-#pragma unroll
-        for (int m = 0; m < DTB; ++m) {
-          tok[m][n] = mma_bf16(aw[m], bx[n], s == 0 ? f32x16{} : tok[m][n]);
-          if constexpr (!QUANT) tok[m][n] = mma_bf16(aw[m], bh[n], tok[m][n]);
-        }
-        uacc[n] = mma_bf16(aw[DTB], bx[n], s == 0 ? f32x16{} : uacc[n]);
-        if constexpr (!QUANT) uacc[n] = mma_bf16(aw[DTB], bh[n], uacc[n]);
-      }
-    }
-  }
-  wave_sync();  // H and X are dead from here on
-
-  // token values relu(acc * scale + bias); value features u[c][sq] to LDS
-  const float* HC = reinterpret_cast<const float*>(smem + C::OFF_HC);
-  {
-#pragma unroll
-    for (int m = 0; m < DTB; ++m)
-#pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int r0 = 32 * m + 8 * jq + 4 * lhi;
-        const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
-        const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
-        const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
-#pragma unroll
-        for (int n = 0; n < 2; ++n)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) tok[m][n][4 * jq + r] = fmaxf(__builtin_fmaf(tok[m][n][4 * jq + r], sv[r], bv[r]), 0.0f);
-      }
-    float* U = reinterpret_cast<float*>(smem + C::OFF_U);
-    const int V = p.value_channels;
-#pragma unroll
-    for (int jq = 0; jq < 4; ++jq) {
-      const int r0 = DD + 8 * jq + 4 * lhi;
-      const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
-      const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
-      const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int ch = 8 * jq + 4 * lhi + r;
-        if (ch < V) {
-#pragma unroll
-          for (int n = 0; n < 2; ++n) {
-            float u = __builtin_fmaf(uacc[n][4 * jq + r], sv[r], bv[r]);
-            if (p.value_conv_relu) u = fmaxf(u, 0.0f);
-            U[ch * 64 + n * 32 + l32] = u;
-          }
-        }
-      }
-    }
-  }
-
-  // Operand fragments from accumulators: K step s of a 128-row accumulator
-  // set X[4][2] (rows = the product's K dimension) for column block n holds
-  // positions 8s .. 8s+7 of the lane's 64 accumulator values.
-  auto frags_of = [&](const f32x16(&X)[DTB][2], int n, int s, bf16x8& hi, bf16x8& lo) {
-    float x[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) x[t] = X[(8 * s + t) / 16][n][(8 * s + t) % 16];
-    split8(x, hi, lo);
-  };
-  // Q^T = Wq tok^T + bq and K^T = Wk tok^T + bk in one pass over the token
-  // fragments (split operands); rows of Q^T and K^T in the token accumulators'
-  // register order, so the token values die as the pass ends
-  f32x16 Qa[DTB][2], Ka[DTB][2];
-  {
-    const uint8_t* qp = static_cast<const uint8_t*>(p.q_w) + (size_t)lane * 16;
-    const uint8_t* kp = static_cast<const uint8_t*>(p.k_w) + (size_t)lane * 16;
-    // A fragments of K step s in ring slot s % 2, loaded one step ahead
-    constexpr int QS = DD / 16, QR = 2;
-    bf16x8 aqr[QR][DTB], akr[QR][DTB];
-    auto load_qk = [&](int st) {
-#pragma unroll
-      for (int m = 0; m < DTB; ++m) {
-        aqr[st % QR][m] = g_frag<MK_BF16>(qp + (st * DTB + m) * 64 * 16);
-        akr[st % QR][m] = g_frag<MK_BF16>(kp + (st * DTB + m) * 64 * 16);
-      }
-    };
-#pragma unroll
-    for (int st = 0; st < QR - 1; ++st) load_qk(st);
-#pragma unroll
-    for (int s = 0; s < QS; ++s) {
-      if (s + QR - 1 < QS) load_qk(s + QR - 1);
-      const bf16x8(&aq)[DTB] = aqr[s % QR];
-      const bf16x8(&ak)[DTB] = akr[s % QR];
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        bf16x8 xh, xl;
-        frags_of(tok, n, s, xh, xl);
-#pragma unroll
-        for (int m = 0; m < DTB; ++m) {
-          Qa[m][n] = mma_bf16(aq[m], xh, s == 0 ? f32x16{} : Qa[m][n]);
-          Qa[m][n] = mma_bf16(aq[m], xl, Qa[m][n]);
-          Ka[m][n] = mma_bf16(ak[m], xh, s == 0 ? f32x16{} : Ka[m][n]);
-          Ka[m][n] = mma_bf16(ak[m], xl, Ka[m][n]);
-        }
-      }
-    }
-#pragma unroll
-    for (int m = 0; m < DTB; ++m)
-#pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int r0 = 32 * m + 8 * jq + 4 * lhi;
-        const float4 bq = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + r0);
-        const float4 bk = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + DD + r0);
-        const float qv[4] = {bq.x, bq.y, bq.z, bq.w}, kv[4] = {bk.x, bk.y, bk.z, bk.w};
-#pragma unroll
-        for (int n = 0; n < 2; ++n)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            Qa[m][n][4 * jq + r] += qv[r];
-            Ka[m][n][4 * jq + r] += kv[r];
-          }
-      }
-  }
-
-  // S[f][t] = sum_d Q[f][d] K[t][d] (hi*hi + hi*lo + lo*hi) and the promotion
-  // offsets O^T[k][t] = sum_d Wp[k][d] K[t][d] for the last row's destinations
-  // action table entries and legal-mask words of the softmax, in flight
-  // during the query-key products
-  constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
-  uint4 tbl[NIT];
-  uint32_t mkw[NIT];
-  {
-    const uint8_t* lg = legal + (size_t)b * NA;
-#pragma unroll
-    for (int i = 0; i < NIT; ++i) {
-      const int a0 = 256 * i + 4 * lane;
-      const bool in = a0 < NA;
-      tbl[i] = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
-      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
-      mkw[i] = in ? mk0 : 0u;
-    }
-  }
-  f32x16 Sa[2][2], Oa;
-  {
-    const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
-    bf16x8 apw[DD / 16];  // every K step's promotion-weight fragment, loaded up front
-#pragma unroll
-    for (int s = 0; s < DD / 16; ++s) apw[s] = g_frag<MK_BF16>(pw + s * 64 * 16);
-#pragma unroll
-    for (int s = 0; s < DD / 16; ++s) {
-      bf16x8 qh[2], ql[2], kh[2], kl[2];
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        frags_of(Qa, n, s, qh[n], ql[n]);
-        frags_of(Ka, n, s, kh[n], kl[n]);
-      }
-#pragma unroll
-      for (int mf = 0; mf < 2; ++mf)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          Sa[mf][nt] = mma_bf16(qh[mf], kh[nt], s == 0 ? f32x16{} : Sa[mf][nt]);
-          Sa[mf][nt] = mma_bf16(qh[mf], kl[nt], Sa[mf][nt]);
-          Sa[mf][nt] = mma_bf16(ql[mf], kh[nt], Sa[mf][nt]);
-        }
-      Oa = mma_bf16(apw[s], kh[1], s == 0 ? f32x16{} : Oa);
-      Oa = mma_bf16(apw[s], kl[1], Oa);
-    }
-  }
-  // logits pre-scaled by log2(e) for the exp2 softmax
-  {
-    const float log2e = 1.4426950408889634f;
-    const float ss = log2e / sqrtf((float)DD);
-    float* S = reinterpret_cast<float*>(smem + C::OFF_S);
-#pragma unroll
-    for (int mf = 0; mf < 2; ++mf)
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int f = 32 * mf + 8 * (v / 4) + 4 * lhi + v % 4, t = 32 * nt + l32;
-          S[f * 64 + t] = Sa[mf][nt][v] * ss;
-        }
-    float* O = reinterpret_cast<float*>(smem + C::OFF_O);
-    if (lhi == 0 && l32 >= 24) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) O[(l32 - 24) * 4 + k] = Oa[k] * log2e;
-    }
-  }
-  wave_sync();
-
-  // ---- legal-action softmax: lane owns the runs of 4 actions at 256 i + 4 lane
-  {
-    const float* S = reinterpret_cast<const float*>(smem + C::OFF_S);
-    const float* O = reinterpret_cast<const float*>(smem + C::OFF_O);
-    float e[NIT][4];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < NIT; ++i) {
-      const int a0 = 256 * i + 4 * lane;
-      const bool in = a0 < NA;  // NA is a multiple of 4
-      const uint4 tb = tbl[i];
-      const uint32_t mk = mkw[i];
-      const uint32_t te[4] = {tb.x, tb.y, tb.z, tb.w};
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t x = te[r], pr = x >> 12;
-        const float z = S[x & 4095u] + (pr ? O[pr - 1] : 0.0f);
-        const bool ok = in && ((mk >> (8 * r)) & 0xffu);
-        e[i][r] = ok ? z : -INFINITY;
-        mx = fmaxf(mx, e[i][r]);
-      }
-    }
-    mx = wave_max(mx);
-    const float msub = mx == -INFINITY ? 0.0f : mx;
-    float sum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < NIT; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        e[i][r] = __builtin_amdgcn_exp2f(e[i][r] - msub);  // exp2(-inf) = 0
-        sum += e[i][r];
-      }
-    sum = wave_sum(sum);
-    const float inv = sum > 0.0f ? 1.0f / sum : 0.0f;
-    float* pol = policy + (size_t)b * NA;
-#pragma unroll
-    for (int i = 0; i < NIT; ++i) {
-      const int a0 = 256 * i + 4 * lane;
-      if (a0 < NA)
-        *reinterpret_cast<float4*>(pol + a0) = make_float4(e[i][0] * inv, e[i][1] * inv, e[i][2] * inv, e[i][3] * inv);
-    }
-  }
-
-  // ---- WDL head: y = relu(W1 u + b1), z = W2 y + b2, softmax, value = W - L
-  {
-    const float* U = reinterpret_cast<const float*>(smem + C::OFF_U);
-    const int H = p.value_hidden, NU = p.value_channels * 64;
-    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
-    for (int k0 = 0; k0 < H; k0 += 64) {
-      const int k = k0 + lane;
-      const bool ok = k < H;
-      const int kk = ok ? k : 0;
-      float y = p.wdl_fc1_b[kk];
-      // fc1 row of unit kk in chunks of 16 inputs, the next chunk in flight
-      // (NU is a multiple of 64)
-      float wa[16], wb[16];
-      auto ld = [&](float(&d)[16], int i0) {
-#pragma unroll
-        for (int t = 0; t < 16; ++t) d[t] = p.wdl_fc1_t[(size_t)(i0 + t) * H + kk];
-      };
-      ld(wa, 0);
-      for (int i0 = 0; i0 < NU; i0 += 32) {
-        ld(wb, i0 + 16);
-#pragma unroll
-        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wa[t], U[i0 + t], y);
-        if (i0 + 32 < NU) ld(wa, i0 + 32);
-#pragma unroll
-        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wb[t], U[i0 + 16 + t], y);
-      }
-      y = ok ? fmaxf(y, 0.0f) : 0.0f;
-      z0 = __builtin_fmaf(p.wdl_fc2_w[kk], y, z0);
-      z1 = __builtin_fmaf(p.wdl_fc2_w[H + kk], y, z1);
-      z2 = __builtin_fmaf(p.wdl_fc2_w[2 * H + kk], y, z2);
-    }
-    z0 = wave_sum(z0) + p.wdl_fc2_b[0];
-    z1 = wave_sum(z1) + p.wdl_fc2_b[1];
-    z2 = wave_sum(z2) + p.wdl_fc2_b[2];
-    const float m = fmaxf(z0, fmaxf(z1, z2));
-    const float e0 = expf(z0 - m), e1 = expf(z1 - m), e2 = expf(z2 - m);
-    const float is = 1.0f / (e0 + e1 + e2);
-    if (lane == 0) {
-      const float pw = e0 * is, pd = e1 * is, pl = e2 * is;
-      value[b] = pw - pl;
-      if (wdl) {
-        wdl[3 * (size_t)b + 0] = pw;
-        wdl[3 * (size_t)b + 1] = pd;
-        wdl[3 * (size_t)b + 2] = pl;
-      }
-    }
-  }
+  dep_heads<MK>(p, smem, legal, policy, value, wdl, b, lane);
 }
 
-}  // namespace
+template <int MK>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1))) void
+az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __restrict__ legal,
+              float* __restrict__ policy, float* __restrict__ value, float* __restrict__ wdl) {
+  using C = DepCfg<MK>;
+  using T = typename C::T;
+  using frag_t = typename T::frag;
+  using acc_t = typename T::acc;
+  using R = Rot<C::RB>;
+  constexpr bool QUANT = C::QUANT;
+  constexpr int RB = C::RB, OFF_H = C::OFF_H, OFF_T = C::OFF_T, OFF_Z = C::OFF_Z;
 
+  __shared__ __attribute__((aligned(16))) uint8_t smem[C::SMEM];
+
+  // Tiles of a layer: five 32-channel blocks x two half-board square blocks.
+  // Wave w (one per SIMD) owns both tiles of block w, and waves 0 and 1 also
+  // tile (4, w), so no SIMD runs more than three of the ten MFMA chains of a K
+  // step.
+  constexpr int NWB = 4;                     // waves per board
+  static_assert(DNMB == NWB + 1, "four waves, five blocks");
+  constexpr int NT = 64 * NWB;
+  constexpr int MBW = 1;                     // blocks whose two tiles the wave owns
+  constexpr int NBW = 2;                     // half-board square blocks
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const int mb0 = wave;                      // first block the wave owns
+  const int b = blockIdx.x;
+  const int Cin = p.in_planes;
+  const float cap = p.act_cap;
+
+  // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
+  for (int i = tid; i < C::ZB / 16; i += NT)
+    *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
+  for (int i = tid; i < DF; i += NT) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
+  {
+    // item k = planes 8k..8k+7 (items wave, wave + NWB, ...): lane = square,
+    // eight coalesced loads, one 16-byte store
+    constexpr int KI = DCP / 8, KW = KI / NWB;
+    static_assert(KI % NWB == 0, "ingest items per wave");
+    float pv[KW][8];
+#pragma unroll
+    for (int kw = 0; kw < KW; ++kw)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int c = 8 * (wave + NWB * kw) + t;
+        const bool ok = c < Cin;
+        const float x = planes[((size_t)b * Cin + (ok ? c : 0)) * 64 + lane];
+        pv[kw][t] = ok ? x : 0.0f;
+      }
+#pragma unroll
+    for (int kw = 0; kw < KW; ++kw) {
+      const int k = wave + NWB * kw;
+      *reinterpret_cast<uint4*>(smem + OFF_T + lane * 128 + ((k ^ swz128(lane)) << 4)) =
+          make_uint4(pack_bf16x2(pv[kw][0], pv[kw][1]), pack_bf16x2(pv[kw][2], pv[kw][3]),
+                     pack_bf16x2(pv[kw][4], pv[kw][5]), pack_bf16x2(pv[kw][6], pv[kw][7]));
+    }
+  }
+
+  // tower weight stream, read through a buffer resource: the lane's offsets
+  // (its own block, and block 4) are constant VGPRs, a step's byte offset is a
+  // scalar and a block's a literal, so the loads cost no vector address
+  // arithmetic.  K step i of the stream lives in ring slot i % NBUF, loaded
+  // NBUF - 1 steps ahead: a wave's K step is two or three MFMAs, so the ring is
+  // deep enough to cover a load from L2 or the Infinity Cache.
+  constexpr int NBUF = 10;
+  static_assert((2 * C::S) % NBUF == 0, "every block's first conv starts at ring slot 0");
+  const __amdgpu_buffer_rsrc_t twr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(p.tower_w), (short)0, (int)(2 * p.blocks * C::LAYER_BYTES), 0x00020000);
+  const int tvoff = (mb0 * 64 + lane) * T::FB;
+  const int tvoffx = ((DNMB - 1) * 64 + lane) * T::FB;
+  // per-layer epilogue constants [bias F | qmul F | pool m F | pool b F] of conv
+  // index k (0 = stem; the pooling constants of conv k - 1): thread-held float4s,
+  // loaded at the start of a layer and parked in LDS before its barrier
+  constexpr int KV = 4 * DF / 4;                     // float4s per slot
+  constexpr int KPL = (KV + NT - 1) / NT;            // per thread
+  auto load_consts = [&](int k, float4(&dst)[KPL]) {
+#pragma unroll
+    for (int t = 0; t < KPL; ++t) {
+      const int i = tid + NT * t, arr = i / (DF / 4), off = 4 * (i % (DF / 4));
+      const float* src = arr == 0 ? p.bias + (size_t)k * DF
+                       : arr == 1 ? (QUANT ? p.qmul + (size_t)k * DF : p.bias)
+                       : arr == 2 ? p.pool_m + (size_t)(k - 1) * DF
+                                  : p.pool_b + (size_t)(k - 1) * DF;
+      dst[t] = i < KV ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto store_consts = [&](int slot, const float4(&v)[KPL]) {
+    float4* dst = reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT);
+#pragma unroll
+    for (int t = 0; t < KPL; ++t)
+      if (tid + NT * t < KV) dst[tid + NT * t] = v[t];
+  };
+  // head constants, staged once: embedding row scale and bias, query and key biases
+  {
+    float* hc = reinterpret_cast<float*>(smem + C::OFF_HC);
+    for (int i = tid; i < AZ_DEP_EMB_ROWS; i += NT) {
+      hc[i] = p.emb_sc[i];
+      hc[AZ_DEP_EMB_ROWS + i] = p.emb_bc[i];
+    }
+    for (int i = tid; i < DD; i += NT) {
+      hc[2 * AZ_DEP_EMB_ROWS + i] = p.q_b[i];
+      hc[2 * AZ_DEP_EMB_ROWS + DD + i] = p.k_b[i];
+    }
+  }
+  {
+    float4 k0[KPL];
+    load_consts(1, k0);
+    store_consts(0, k0);
+  }
+  __syncthreads();
+
+  // ---- stem and tower of one wave.  XN >= 0: the wave also owns tile (4, XN).
+  // Fragment / accumulator set m < MBW is block mb0 + m (both tiles); set MBW,
+  // when present, is block 4 (tile XN only).  Every wave meets the same
+  // sequence of workgroup barriers.
+  auto trunk = [&](auto xn_c) {
+    constexpr int XN = decltype(xn_c)::value;
+    constexpr int NAF = MBW + (XN >= 0 ? 1 : 0);   // weight fragments per K step
+    auto blk_of = [&](int m) { return m < MBW ? mb0 + m : DNMB - 1; };
+    auto n_lo = [](int m) constexpr { return m < MBW ? 0 : XN; };
+    auto n_hi = [](int m) constexpr { return m < MBW ? NBW : XN + 1; };
+
+    // residual stream of the board (bf16 networks): h = hi + lo, hi = bf16(h) in
+    // the H buffer (the convolution operand), lo = bf16(h - hi) packed here, two
+    // per register: [set][half][run of 4 channels][2]
+    uint32_t rlo[QUANT ? 1 : NAF][QUANT ? 1 : NBW][QUANT ? 1 : 8];
+
+    frag_t A[NBUF][NAF];
+    auto load_step = [&](frag_t(&dst)[NAF], int soff) {
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+        dst[m] = __builtin_bit_cast(frag_t, __builtin_amdgcn_raw_buffer_load_b128(twr, tvoff, soff + m * 64 * T::FB, 0));
+      if constexpr (NAF > MBW)
+        dst[MBW] = __builtin_bit_cast(frag_t, __builtin_amdgcn_raw_buffer_load_b128(twr, tvoffx, soff, 0));
+    };
+
+    // ---- stem: bf16 3x3 conv over 64 (padded) input channels, K = 576
+    {
+      constexpr int SSTEP = DNMB * 64 * 16;  // bytes per K step of the stem stream
+      const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)lane * 16;
+      f32x16 sacc[NAF][NBW];
+      // 36 K steps (tap = st / 4, 16 channels each): A fragments of step st in ring
+      // slot st % 4, loaded three steps ahead; B fragments one step ahead
+      constexpr int SR = 4, NST = 9 * DCP / 16;
+      bf16x8 a[SR][NAF];
+      auto load_a = [&](int st) {
+#pragma unroll
+        for (int m = 0; m < NAF; ++m) a[st % SR][m] = g_frag<MK_BF16>(sw8 + st * SSTEP + blk_of(m) * 64 * 16);
+      };
+      auto load_b = [&](int st, bf16x8(&dst)[NBW]) {
+        const int tap = st / 4, cs = st % 4, dy = tap / 3 - 1, dx = tap % 3 - 1;
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) {
+          const int j = n * 32 + l32, r = (j >> 3) + dy, c = (j & 7) + dx;
+          const bool ok = (unsigned)r < 8u && (unsigned)c < 8u;
+          const int src = r * 8 + c;
+          const int row = ok ? OFF_T + src * 128 : OFF_Z + ((src * 128) & 255);
+          dst[n] = *reinterpret_cast<const bf16x8*>(smem + row + (((2 * cs + lhi) ^ swz128(src)) << 4));
+        }
+      };
+#pragma unroll
+      for (int st = 0; st < SR - 1; ++st) load_a(st);
+      bf16x8 bcur[NBW], bnext[NBW];
+      load_b(0, bcur);
+#pragma unroll
+      for (int st = 0; st < NST; ++st) {
+        if (st + SR - 1 < NST) load_a(st + SR - 1);
+        if (st + 1 < NST) load_b(st + 1, bnext);
+#pragma unroll
+        for (int m = 0; m < NAF; ++m)
+#pragma unroll
+          for (int n = n_lo(m); n < n_hi(m); ++n)
+            sacc[m][n] = mma_bf16(a[st % SR][m], bcur[n], st == 0 ? f32x16{} : sacc[m][n]);
+#pragma unroll
+        for (int n = 0; n < NBW; ++n) bcur[n] = bnext[n];
+      }
+      // the tower's first weight steps, in flight during the stem's epilogue
+      static_for<0, NBUF - 1>([&](auto i_c) {
+        constexpr int i = decltype(i_c)::value;
+        load_step(A[i], i * C::STEP_BYTES);
+      });
+      // epilogue: bias, activation (codes for int8), store in the tower format at OFF_H
+#pragma unroll
+      for (int m = 0; m < NAF; ++m)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int ch0 = blk_of(m) * 32 + 8 * q + 4 * lhi;
+          const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
+          float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
+          if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
+#pragma unroll
+          for (int n = n_lo(m); n < n_hi(m); ++n) {
+            const int j = n * 32 + l32;
+            const f32x16& v = sacc[m][n];
+            if constexpr (!QUANT) {
+              const float y0 = act_fn(v[4 * q + 0] + bb.x, cap), y1 = act_fn(v[4 * q + 1] + bb.y, cap);
+              const float y2 = act_fn(v[4 * q + 2] + bb.z, cap), y3 = act_fn(v[4 * q + 3] + bb.w, cap);
+              rlo[m][n][2 * q + 0] = pack_bf16x2(y0 - bf16_round(y0), y1 - bf16_round(y1));
+              rlo[m][n][2 * q + 1] = pack_bf16x2(y2 - bf16_round(y2), y3 - bf16_round(y3));
+              *reinterpret_cast<uint2*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi) =
+                  make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+            } else {
+              const float hi = p.qhi[0];
+              const float z0 = med3(__builtin_fmaf(v[4 * q + 0], mm.x, bb.x), 0.0f, hi);
+              const float z1 = med3(__builtin_fmaf(v[4 * q + 1], mm.y, bb.y), 0.0f, hi);
+              const float z2 = med3(__builtin_fmaf(v[4 * q + 2], mm.z, bb.z), 0.0f, hi);
+              const float z3 = med3(__builtin_fmaf(v[4 * q + 3], mm.w, bb.w), 0.0f, hi);
+              *reinterpret_cast<uint32_t*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15)) =
+                  pack_codes<MK>(z0, z1, z2, z3);
+            }
+          }
+        }
+    }
+    __syncthreads();
+
+    // ---- residual tower
+    {
+      constexpr int CPT = C::CPT;
+      acc_t c[NAF][NBW];
+      const int nconv = 2 * p.blocks;
+
+      const int l32_ = l32, lhi_ = lhi;
+      auto conv = [&](auto second_c, auto pool_c, auto lb_c, int n_conv) {
+        constexpr bool SECOND = decltype(second_c)::value;
+        constexpr bool POOL = decltype(pool_c)::value;   // first conv of a pooling block
+        constexpr int LB = decltype(lb_c)::value;        // ring slot of the layer's first step
+        // lane coordinates, opaque to the compiler per layer, so that the layer's
+        // many lane-dependent addresses are computed in the layer instead of being
+        // hoisted out of the block loop and held (or spilled) across it
+        int l32 = l32_, lhi = lhi_;
+        asm volatile("" : "+v"(l32), "+v"(lhi));
+        const int wl = n_conv * (int)C::LAYER_BYTES;  // byte offset of the layer in the stream
+        const bool has_next = n_conv + 1 < nconv;
+        const int in_off = SECOND ? OFF_T : OFF_H;
+        const int out_off = SECOND ? OFF_H : OFF_T;
+        const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
+        // the next layer's epilogue constants, in flight during this layer
+        float4 kn[KPL];
+        if (has_next) load_consts(n_conv + 2, kn);
+        // B fragments of one K step.  Channel step cs reads logical chunk
+        // lc = 2 cs + lhi of the tap's row, at chunk position (lc + rot) mod NC with
+        // rot the row's rotation: from a per-tap base b0 = row + 16 (lhi + rot) the
+        // address is b0 + 32 cs, except for the last steps, where lc + rot can pass
+        // the row's end and the base is chosen per lane once per tap.
+        constexpr int WRAP0 = (R::NC - 1 - R::RM) / 2;  // first step that can wrap
+        constexpr int NWRAP = CPT > WRAP0 ? CPT - WRAP0 : 0;
+        struct TapRows {
+          int b0[NBW];
+          int bw[NBW][NWRAP > 0 ? NWRAP : 1];
+        };
+        TapRows row, nrow;
+        auto rows_for = [&](int tap, TapRows& tr) {
+          const int dy = tap / 3 - 1, dx = tap % 3 - 1;
+#pragma unroll
+          for (int n = 0; n < NBW; ++n) {
+            const int j = n * 32 + l32, r = (j >> 3) + dy, cc = (j & 7) + dx;
+            const bool ok = (unsigned)r < 8u && (unsigned)cc < 8u;
+            const int src = r * 8 + cc;
+            const int ra = in_off + src * RB, rz = OFF_Z + ((src * RB) & 255);
+            const int msk = -(int)ok;
+            const int x = lhi + R::sw(src);
+            tr.b0[n] = ((ra & msk) | (rz & ~msk)) + 16 * x;
+#pragma unroll
+            for (int k = 0; k < NWRAP; ++k)
+              tr.bw[n][k] = tr.b0[n] - (2 * (WRAP0 + k) + x >= R::NC ? 16 * R::NC : 0);
+          }
+        };
+        auto load_b = [&](const TapRows& tr, auto cs_c, frag_t(&dst)[NBW]) {
+          constexpr int cs = decltype(cs_c)::value;
+#pragma unroll
+          for (int n = 0; n < NBW; ++n) {
+            int base;
+            if constexpr (cs >= WRAP0) base = tr.bw[n][cs - WRAP0];
+            else base = tr.b0[n];
+            dst[n] = *reinterpret_cast<const frag_t*>(smem + base + 32 * cs);
+          }
+        };
+        frag_t bc[NBW], bn[NBW];
+        rows_for(0, row);
+        load_b(row, std::integral_constant<int, 0>{}, bc);
+
+        // one tap: CPT K steps; R0 = ring slot of its first step
+        auto tap_body = [&](auto r0_c, auto first_c, int tap) {
+          constexpr int R0 = decltype(r0_c)::value;
+          constexpr bool FIRST = decltype(first_c)::value;
+          rows_for(tap + 1, nrow);
+          static_for<0, CPT>([&](auto cs_c) {
+            constexpr int cs = decltype(cs_c)::value;
+            constexpr int cur = (R0 + cs) % NBUF;
+            {
+              // step tap*CPT + cs + NBUF-1 of this layer (of the next layer past its end;
+              // past the network's last layer this layer is re-read and never used)
+              const int gi = tap * CPT + cs + NBUF - 1;
+              load_step(A[(cur + NBUF - 1) % NBUF], wl + ((has_next || gi < C::S) ? gi * C::STEP_BYTES : 0));
+            }
+            if constexpr (cs + 1 < CPT) load_b(row, std::integral_constant<int, cs + 1>{}, bn);
+            else load_b(nrow, std::integral_constant<int, 0>{}, bn);
+#pragma unroll
+            for (int m = 0; m < NAF; ++m)
+#pragma unroll
+              for (int n = n_lo(m); n < n_hi(m); ++n)
+                c[m][n] = T::mma(A[cur][m], bc[n], (FIRST && cs == 0) ? acc_t{} : c[m][n]);
+#pragma unroll
+            for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
+            // each MFMA followed by one of the next step's LDS reads, then by one of
+            // the prefetched step's weight loads
+            static_for<0, MBW * NBW + NAF - MBW>([&](auto i_c) {
+              constexpr int i = decltype(i_c)::value;
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              if constexpr (i < NBW) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+              if constexpr (i < NAF) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            });
+          });
+          row = nrow;
+        };
+        constexpr int U = NBUF / gcd_c(CPT, NBUF), NIT = 8 / U, REM = 8 % U;
+        tap_body(std::integral_constant<int, LB>{}, std::true_type{}, 0);
+#pragma nounroll
+        for (int it = 0; it < NIT; ++it) {
+          static_for<0, U>([&](auto u_c) {
+            constexpr int u = decltype(u_c)::value;
+            tap_body(std::integral_constant<int, (LB + (1 + u) * CPT) % NBUF>{}, std::false_type{}, 1 + it * U + u);
+          });
+        }
+        static_for<0, REM>([&](auto u_c) {
+          constexpr int u = decltype(u_c)::value, t = 1 + NIT * U + u;
+          tap_body(std::integral_constant<int, (LB + t * CPT) % NBUF>{}, std::false_type{}, t);
+        });
+
+        // global pooling: pooled channels' board mean and maximum, projection to
+        // the regular channels' biases (LDS OFF_C)
+        float cinv = 1.0f;
+        if constexpr (POOL) {
+          cinv = p.pool_cinv[n_conv];
+          // (1) pooled activations to LDS as [pooled channel][square] f32 in the T
+          //     buffer (written by this layer's epilogue only afterwards); rows of
+          //     256 bytes with 16-byte chunks XOR-swizzled by the row
+          float* pt = reinterpret_cast<float*>(smem + OFF_T);
+          static_assert(DG * 64 * 4 <= C::BUF, "pooled activations fit in the T buffer");
+          static_for<0, NAF * 4>([&](auto k_c) {
+            constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4;
+            if (32 * blk_of(m) + 8 * q >= DFR) {
+              const int ch0 = 32 * blk_of(m) + 8 * q + 4 * lhi;
+              const float4 mm = *reinterpret_cast<const float4*>(kslot + 2 * DF + ch0);
+              const float4 bb = *reinterpret_cast<const float4*>(kslot + 3 * DF + ch0);
+              const float mv[4] = {mm.x, mm.y, mm.z, mm.w}, bv[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int pc = ch0 + r - DFR;
+#pragma unroll
+                for (int n = n_lo(m); n < n_hi(m); ++n) {
+                  const int sq = 32 * n + l32;
+                  pt[pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3)] =
+                      med3(__builtin_fmaf((float)c[m][n][4 * q + r], mv[r], bv[r]), 0.0f, cap);
+                }
+              }
+            }
+          });
+          wave_lds_sync();
+          // (2) wave 0, lane pc < g: board sum (fp64) and maximum of its row;
+          //     g = [mean, max]
+          double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
+          if (wave == 0 && lane < DG) {
+            double sum = 0.0;
+            float mx = 0.0f;  // activations are >= 0
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+              const float4 v = *reinterpret_cast<const float4*>(pt + lane * 64 + ((j ^ (lane & 15)) << 2));
+              sum += (double)v.x;
+              sum += (double)v.y;
+              sum += (double)v.z;
+              sum += (double)v.w;
+              mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+            }
+            pg[lane] = sum * (1.0 / 64.0);
+            pg[DG + lane] = (double)mx;
+          }
+          wave_lds_sync();
+          // (3) c[o] = sum_i Wg[o][i] g[i] in fp64 (fp32 weights are exact): waves 0
+          //     and 1 take output 64 wave + lane; the weights, [i/4][o][4] floats,
+          //     stream in chunks of 16 inputs with the next chunk in flight
+          if (wave < 2) {
+            const int o = 64 * wave + lane;
+            const float4* wt = reinterpret_cast<const float4*>(p.pool_wt) +
+                               (size_t)(n_conv / 2 / p.pool_every) * (2 * DG / 4) * AZ_DEP_POOL_OPAD + o;
+            constexpr int NCH = 2 * DG / 16;
+            float4 wbuf[2][4];
+            auto load_chunk = [&](float4(&dst)[4], int chk) {
+#pragma unroll
+              for (int k4 = 0; k4 < 4; ++k4) dst[k4] = wt[(size_t)(4 * chk + k4) * AZ_DEP_POOL_OPAD];
+            };
+            load_chunk(wbuf[0], 0);
+            double co = 0.0;
+#pragma unroll
+            for (int chk = 0; chk < NCH; ++chk) {
+              if (chk + 1 < NCH) load_chunk(wbuf[(chk + 1) & 1], chk + 1);
+#pragma unroll
+              for (int k4 = 0; k4 < 4; ++k4) {
+                const float4 w = wbuf[chk & 1][k4];
+                const double* gi = pg + 16 * chk + 4 * k4;
+                co = __builtin_fma((double)w.x, gi[0], co);
+                co = __builtin_fma((double)w.y, gi[1], co);
+                co = __builtin_fma((double)w.z, gi[2], co);
+                co = __builtin_fma((double)w.w, gi[3], co);
+              }
+            }
+            if (o < DFR) reinterpret_cast<float*>(smem + C::OFF_C)[o] = (float)co;
+          }
+          wave_lds_sync();
+        }
+
+        // epilogue: per run of 4 channels; LDS reads of constants (and residual
+        // codes) issued two runs ahead
+        float hi = 0.0f, rq = 0.0f;
+        if constexpr (QUANT) {
+          hi = p.qhi[n_conv + 1];
+          rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
+        }
+        constexpr int NRUN = NAF * 4, EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
+        constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
+        constexpr bool RHI = !QUANT && SECOND;    // residual hi parts, read in place
+        float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
+        uint32_t rcode[RCODE ? EP_RING : 1][NBW];
+        uint2 rhi[RHI ? EP_RING : 1][NBW];
+        auto ep_addr = [&](int m, int q, int n) {
+          const int j = n * 32 + l32;
+          const int ch0 = blk_of(m) * 32 + 8 * q + 4 * lhi;
+          const int rowo = out_off + j * RB;
+          if constexpr (QUANT) return rowo + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15);
+          else return rowo + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi;
+        };
+        auto ep_load = [&](auto k_c) {
+          constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
+          const int ch0 = blk_of(m) * 32 + 8 * q + 4 * lhi;
+          kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
+          if constexpr (QUANT) km[slot] = *reinterpret_cast<const float4*>(kslot + DF + ch0);
+          if constexpr (POOL) kc[slot] = *reinterpret_cast<const float4*>(smem + C::OFF_C + ch0 * 4);
+          if constexpr (RCODE) {
+#pragma unroll
+            for (int n = n_lo(m); n < n_hi(m); ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
+          }
+          if constexpr (RHI) {
+#pragma unroll
+            for (int n = n_lo(m); n < n_hi(m); ++n) rhi[slot][n] = *reinterpret_cast<const uint2*>(smem + ep_addr(m, q, n));
+          }
+        };
+        static_for<0, EP_AHEAD>([&](auto k_c) { ep_load(k_c); });
+        static_for<0, NRUN>([&](auto k_c) {
+          constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
+          if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
+          const float4 bb = kb[slot];
+#pragma unroll
+          for (int n = n_lo(m); n < n_hi(m); ++n) {
+            const int addr = ep_addr(m, q, n);
+            const acc_t& v = c[m][n];
+            if constexpr (!QUANT) {
+              float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
+              float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
+              if constexpr (POOL) {
+                const float4 cc = kc[slot];
+                y0 += cc.x;
+                y1 += cc.y;
+                y2 += cc.z;
+                y3 += cc.w;
+              }
+              if constexpr (SECOND) {
+                // block input h = hi + lo (exact in fp32)
+                const uint2 hv = rhi[slot][n];
+                const uint32_t l01 = rlo[m][n][2 * q], l23 = rlo[m][n][2 * q + 1];
+                y0 = act_fn(y0 + (__uint_as_float(hv.x << 16) + __uint_as_float(l01 << 16)), cap);
+                y1 = act_fn(y1 + (__uint_as_float(hv.x & 0xffff0000u) + __uint_as_float(l01 & 0xffff0000u)), cap);
+                y2 = act_fn(y2 + (__uint_as_float(hv.y << 16) + __uint_as_float(l23 << 16)), cap);
+                y3 = act_fn(y3 + (__uint_as_float(hv.y & 0xffff0000u) + __uint_as_float(l23 & 0xffff0000u)), cap);
+                rlo[m][n][2 * q + 0] = pack_bf16x2(y0 - bf16_round(y0), y1 - bf16_round(y1));
+                rlo[m][n][2 * q + 1] = pack_bf16x2(y2 - bf16_round(y2), y3 - bf16_round(y3));
+              } else {
+                y0 = act_fn(y0, cap);
+                y1 = act_fn(y1, cap);
+                y2 = act_fn(y2, cap);
+                y3 = act_fn(y3, cap);
+              }
+              *reinterpret_cast<uint2*>(smem + addr) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+            } else {
+              const float4 mm = km[slot];
+              float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
+              float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
+              float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
+              float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
+              if constexpr (POOL) {
+                const float4 cc = kc[slot];
+                z0 = __builtin_fmaf(cc.x, cinv, z0);
+                z1 = __builtin_fmaf(cc.y, cinv, z1);
+                z2 = __builtin_fmaf(cc.z, cinv, z2);
+                z3 = __builtin_fmaf(cc.w, cinv, z3);
+              }
+              if constexpr (SECOND) {
+                const uint32_t r = rcode[slot][n];
+                z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
+                z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
+                z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
+                z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
+              }
+              *reinterpret_cast<uint32_t*>(smem + addr) =
+                  pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi), med3(z3, 0.0f, hi));
+            }
+          }
+        });
+        if (has_next) store_consts((n_conv + 1) & 1, kn);
+        __syncthreads();
+      };
+
+      for (int blk = 0; blk < p.blocks; ++blk) {
+        const bool pool = p.pool_every > 0 && blk % p.pool_every == p.pool_every - 1;
+        if (pool) conv(std::false_type{}, std::true_type{}, std::integral_constant<int, 0>{}, 2 * blk);
+        else conv(std::false_type{}, std::false_type{}, std::integral_constant<int, 0>{}, 2 * blk);
+        conv(std::true_type{}, std::false_type{}, std::integral_constant<int, C::S % NBUF>{}, 2 * blk + 1);
+      }
+    }
+
+    // ---- heads input (bf16 networks): the low part h - bf16(h) of the fp32
+    // residual as bf16 rows [square][F] at OFF_X, H holding bf16(h); int8
+    // networks read the final codes from H and convert them in registers
+    if constexpr (!QUANT) {
+      using RX = Rot<C::RBX>;
+#pragma unroll
+      for (int m = 0; m < NAF; ++m)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int ch0 = blk_of(m) * 32 + 8 * q + 4 * lhi;
+#pragma unroll
+          for (int n = n_lo(m); n < n_hi(m); ++n) {
+            const int j = n * 32 + l32;
+            *reinterpret_cast<uint2*>(smem + C::OFF_X + j * C::RBX + (RX::pos(ch0 >> 3, RX::sw(j)) << 4) + 8 * lhi) =
+                make_uint2(rlo[m][n][2 * q], rlo[m][n][2 * q + 1]);
+          }
+        }
+    }
+  };
+  if (wave == 0) trunk(std::integral_constant<int, 0>{});
+  else if (wave == 1) trunk(std::integral_constant<int, 1>{});
+  else trunk(std::integral_constant<int, -1>{});
+  __syncthreads();
+  // ---- heads: wave 0
+  if (wave == 0) dep_heads<MK>(p, smem, legal, policy, value, wdl, b, lane);
+}
+
+
+}  // namespace

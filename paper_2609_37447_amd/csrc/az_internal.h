@@ -78,16 +78,19 @@ struct AzDevNet {
 #define AZ_DEP_POOL_OPAD 128
 #define AZ_DEP_ACTION_SLOTS 2048
 #define AZ_DEP_MAX_IN_PLANES 64
+// Largest batch for which the deployed network runs four waves per board by default
+#define AZ_DEP_SMALL_MAX_BATCH 256
 
 // Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small, 3 = medium.
 hipError_t az_launch_mfma(int dtype, int tiling, const AzDevNet& net, const float* planes,
                           const uint8_t* legal, int B, float* policy, float* value,
                           hipStream_t stream);
-// Deployed network (F = 160) in int8 or bf16; wdl may be NULL.
-hipError_t az_launch_deployed_int8(const AzDevNet& net, const float* planes, const uint8_t* legal, int B,
-                                   float* policy, float* value, float* wdl, hipStream_t stream);
-hipError_t az_launch_deployed_bf16(const AzDevNet& net, const float* planes, const uint8_t* legal, int B,
-                                   float* policy, float* value, float* wdl, hipStream_t stream);
+// Deployed network (F = 160) in int8 or bf16; wdl may be NULL.  tiling: 1 = one
+// wave per board, 2 = four waves per board.
+hipError_t az_launch_deployed_int8(const AzDevNet& net, int tiling, const float* planes, const uint8_t* legal,
+                                   int B, float* policy, float* value, float* wdl, hipStream_t stream);
+hipError_t az_launch_deployed_bf16(const AzDevNet& net, int tiling, const float* planes, const uint8_t* legal,
+                                   int B, float* policy, float* value, float* wdl, hipStream_t stream);
 hipError_t az_launch_f32(const AzDevNet& net, const float* planes, const uint8_t* legal, int B,
                          float* policy, float* value, hipStream_t stream);
 // Boards per workgroup of a tiling (for grid sizing and tests).

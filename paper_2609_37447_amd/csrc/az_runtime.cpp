@@ -345,9 +345,13 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // below a few hundred boards; at 1024 boards the four-board large tiling wins
 // for bf16 and fp8, and the two-board medium tiling (two workgroups per compute
 // unit) ties with it for int8.
+//
+// Deployed network: four waves per board while the batch leaves compute units
+// idle (up to one board per compute unit), one wave per board beyond.
 int choose_tiling(const az_net* n, int B) {
-  if (n->dtype == AZ_F32 || is_deployed(n->spec)) return 0;
+  if (n->dtype == AZ_F32) return 0;
   if (n->tiling) return n->tiling;
+  if (is_deployed(n->spec)) return B <= AZ_DEP_SMALL_MAX_BATCH ? 2 : 1;
   const int F = n->spec.filters;
   if (B < 512) return 2;
   if (n->dtype == AZ_BF16) return B >= 1024 ? 1 : 2;
@@ -672,8 +676,8 @@ int az_eval_batch_wdl(az_net* net, const float* planes, const uint8_t* legal, in
   if (cur != net->device && (e = hipSetDevice(net->device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dep)
-    e = (net->dtype == AZ_INT8 ? az_launch_deployed_int8 : az_launch_deployed_bf16)(net->dn, planes, legal, B,
-                                                                                     policy, value, wdl, s);
+    e = (net->dtype == AZ_INT8 ? az_launch_deployed_int8 : az_launch_deployed_bf16)(
+        net->dn, choose_tiling(net, B), planes, legal, B, policy, value, wdl, s);
   else if (net->dtype == AZ_F32)
     e = az_launch_f32(net->dn, planes, legal, B, policy, value, s);
   else
@@ -695,9 +699,9 @@ int az_net_moves(const az_net* net) {
 
 int az_net_set_tiling(az_net* net, int32_t tiling) {
   if (!net) return fail(AZ_ERR_INVALID_ARG, "NULL handle");
-  const bool valid = (net->dtype == AZ_F32 || is_deployed(net->spec))
-                         ? tiling == 0
-                         : (tiling == 0 || az_mfma_tiling_valid(net->spec.filters, tiling));
+  const bool valid = net->dtype == AZ_F32          ? tiling == 0
+                     : is_deployed(net->spec)          ? (tiling >= 0 && tiling <= 2)
+                                                       : (tiling == 0 || az_mfma_tiling_valid(net->spec.filters, tiling));
   if (!valid)
     return fail(AZ_ERR_INVALID_ARG, "tiling %d not available for this dtype", tiling);
   net->tiling = tiling;

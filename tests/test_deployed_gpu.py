@@ -6,7 +6,8 @@ int8 (the paper's deployment: int8 trunk with the fixed ReLU6 activation scale
 6/127, per-output-channel weight scales, pooling and heads in floating point)
 is compared with the oracle's int8 network; bf16 with the float64 network.
 Tolerances: int8 max |dP| 3e-2 and |dV| 5e-2, bf16 1e-2 and 2e-2 (the WDL
-probabilities are held to the value tolerance)."""
+probabilities are held to the value tolerance).  Both kernel tilings (one wave
+per board, four waves per board) are run and must agree bitwise."""
 
 import numpy as np
 import pytest
@@ -52,7 +53,7 @@ def _scales(shape, blob):
     return OD.weight_scales(shape, blob), np.full(2 * shape.blocks + 1, RELU6_SCALE, np.float32)
 
 
-def gpu_eval(shape, blob, dtype, planes, legal, ws=None, acs=None):
+def gpu_eval(shape, blob, dtype, planes, legal, ws=None, acs=None, tiling=0):
     import torch
 
     import paper_2609_37447_amd as az
@@ -60,6 +61,8 @@ def gpu_eval(shape, blob, dtype, planes, legal, ws=None, acs=None):
     net = az.az_net_load(az.spec_from_shape(shape, B), blob, dtype, ws, acs)
     try:
         assert az.az_net_moves(net) == 1880
+        az.az_net_set_tiling(net, tiling)
+        print(f"case {dtype} blocks={shape.blocks} B={B} tiling={tiling or az.az_net_tiling_for(net, B)}", flush=True)
         dev = torch.device("cuda:0")
         pl = torch.from_numpy(np.ascontiguousarray(planes, dtype=np.float32)).to(dev)
         lg = torch.from_numpy(np.ascontiguousarray(legal, dtype=np.uint8)).to(dev)
@@ -90,14 +93,15 @@ def _check(got, ref, legal, dtype):
     return dp, dv
 
 
+@pytest.mark.parametrize("tiling", [1, 2])
 @pytest.mark.parametrize("blocks,B", [(2, 13), (4, 37)])
-def test_deployed_int8_matches_quantised_oracle(blocks, B):
+def test_deployed_int8_matches_quantised_oracle(blocks, B, tiling):
     shape = _shape(blocks)
     blob = azgen.make_weights(shape, 1006, alpha_fold=True, bf16=True)
     planes, legal = _inputs(shape, B, 2006 + blocks)
     legal = _edge_rows(legal)
     ws, acs = _scales(shape, blob)
-    got = gpu_eval(shape, blob, "int8", planes, legal, ws, acs)
+    got = gpu_eval(shape, blob, "int8", planes, legal, ws, acs, tiling=tiling)
     ref = OD.forward_quant(shape, blob, ws, acs, planes, legal)
     _check(got, ref, legal, "int8")
 
@@ -114,25 +118,27 @@ def test_deployed_int8_literal_heads():
     _check(got, ref, legal, "int8")
 
 
+@pytest.mark.parametrize("tiling", [1, 2])
 @pytest.mark.parametrize("blocks,B", [(2, 11), (3, 20)])
-def test_deployed_bf16_matches_float_oracle(blocks, B):
+def test_deployed_bf16_matches_float_oracle(blocks, B, tiling):
     shape = _shape(blocks)
     blob = azgen.make_weights(shape, 1006, alpha_fold=True, bf16=True)
     planes, legal = _inputs(shape, B, 2106 + blocks)
     legal = _edge_rows(legal)
-    got = gpu_eval(shape, blob, "bf16", planes, legal)
+    got = gpu_eval(shape, blob, "bf16", planes, legal, tiling=tiling)
     ref = OD.forward(shape, blob, planes, legal)
     _check(got, ref, legal, "bf16")
 
 
-def test_deployed_no_pooling_and_other_shapes():
+@pytest.mark.parametrize("tiling", [1, 2])
+def test_deployed_no_pooling_and_other_shapes(tiling):
     # pooling switched off, 20 input planes, 5 value channels, 100 hidden units,
     # no ReLU after the value convolution, uncapped activation
     shape = _shape(2, in_planes=20, pool_every=0, value_channels=5, value_hidden=100, value_conv_relu=0,
                    act_cap=0.0)
     blob = azgen.make_weights(shape, 1016, alpha_fold=True, bf16=True)
     planes, legal = _inputs(shape, 9, 2116)
-    got = gpu_eval(shape, blob, "bf16", planes, legal)
+    got = gpu_eval(shape, blob, "bf16", planes, legal, tiling=tiling)
     ref = OD.forward(shape, blob, planes, legal)
     _check(got, ref, legal, "bf16")
 
@@ -160,6 +166,36 @@ def test_deployed_14x160_bf16_sampled_rows():
     _check((Pg[rows], Vg[rows], Wg[rows]), ref, legal[rows], "bf16")
 
 
+@pytest.mark.parametrize("dtype,B", [("int8", 64), ("int8", 256), ("bf16", 64)])
+def test_deployed_14x160_small_batch_sampled_rows(dtype, B):
+    # the interactive regime: the default tiling below 257 boards is four waves per board
+    w = azgen.WORKLOADS[f"deployed14x160_{dtype}_b1024"]
+    blob = azgen.workload_weights(w)
+    planes, legal = azgen.make_inputs(w, n=B)
+    ws, acs = _scales(w.shape, blob) if dtype == "int8" else (None, None)
+    Pg, Vg, Wg = gpu_eval(w.shape, blob, dtype, planes, legal, ws, acs)
+    assert_policy_structure(Pg, legal)
+    rows = np.r_[0:8, B - 8:B]
+    ref = (OD.forward_quant(w.shape, blob, ws, acs, planes[rows], legal[rows]) if dtype == "int8"
+           else OD.forward(w.shape, blob, planes[rows], legal[rows]))
+    _check((Pg[rows], Vg[rows], Wg[rows]), ref, legal[rows], dtype)
+
+
+@pytest.mark.parametrize("dtype", ["int8", "bf16"])
+def test_deployed_tilings_agree_bitwise(dtype):
+    # every tile's K sums run in the same order in both tilings, and the pooling
+    # projection and the heads are the same code: identical outputs
+    shape = _shape(4)
+    blob = azgen.make_weights(shape, 1056, alpha_fold=True, bf16=True)
+    planes, legal = _inputs(shape, 21, 2256)
+    legal = _edge_rows(legal)
+    ws, acs = _scales(shape, blob) if dtype == "int8" else (None, None)
+    one = gpu_eval(shape, blob, dtype, planes, legal, ws, acs, tiling=1)
+    four = gpu_eval(shape, blob, dtype, planes, legal, ws, acs, tiling=2)
+    for a, b in zip(one, four):
+        assert np.array_equal(a, b)
+
+
 def test_deployed_rows_do_not_depend_on_the_batch():
     shape = _shape(2)
     blob = azgen.make_weights(shape, 1006, alpha_fold=True, bf16=True)
@@ -171,15 +207,18 @@ def test_deployed_rows_do_not_depend_on_the_batch():
         assert np.array_equal(a[5:6], b)
 
 
-def test_deployed_has_a_single_tiling():
+def test_deployed_tiling_choice():
+    # four waves per board up to 256 boards (one per compute unit), one wave beyond
     import paper_2609_37447_amd as az
     shape = _shape(2)
     blob = azgen.make_weights(shape, 1036, alpha_fold=True, bf16=True)
-    net = az.az_net_load(az.spec_from_shape(shape, 64), blob, "bf16")
+    net = az.az_net_load(az.spec_from_shape(shape, 1024), blob, "bf16")
     try:
-        assert az.az_net_tiling_for(net, 64) == 0
-        assert az.az_net_set_tiling(net, 0) == az.AZ_OK
-        for t in (1, 2, 3):
+        assert [az.az_net_tiling_for(net, B) for B in (1, 64, 256, 257, 1024)] == [2, 2, 2, 1, 1]
+        for t in (0, 1, 2):
+            assert az.az_net_set_tiling(net, t) == az.AZ_OK
+        assert az.az_net_tiling_for(net, 1024) == 2
+        for t in (3, -1):
             assert az.az_net_set_tiling(net, t, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
     finally:
         az.az_net_free(net)
