@@ -48,11 +48,13 @@ def kernel_source(shape):
 # copy kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  An entry holds
 # for the kernel source it was taken on only: any other source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
-TRAFFIC = {  # (workload, tiling): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    ("net20x128_int8_b1024", 3): ("faf2c3970238b8113f568cabf1e9363b742d350fdec26bd0ffc19cbf57c667f6",
-                                  33413.4, 18704.0),
-    ("deployed14x160_int8_b1024", 0): ("24082077b51b53ce5cef9da3fc21122d80028dd2839eb0235160b812ec79a625",
-                                       46261.5, 30204.2),
+TRAFFIC = {  # (workload, tiling, batch): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
+    ("net20x128_int8_b1024", 3, 1024): ("faf2c3970238b8113f568cabf1e9363b742d350fdec26bd0ffc19cbf57c667f6",
+                                        33413.4, 18704.0),
+    ("deployed14x160_int8_b1024", 1, 1024): ("0492418980244a44ad54fdece8376f64984a685d3a1d41e624a5846f823d4940",
+                                             46066.0, 29226.5),
+    ("deployed14x160_int8_b1024", 2, 64): ("0492418980244a44ad54fdece8376f64984a685d3a1d41e624a5846f823d4940",
+                                           29836.8, 1736.0),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
@@ -100,9 +102,9 @@ def roofline_peak(shape, dtype):
     return sum(flop.values()), sum(flop.values()) / t_floor
 
 
-def traffic_bytes(w, tiling):
+def traffic_bytes(w, tiling, B):
     """Scaled HBM bytes per launch, or None without counters for this exact kernel."""
-    e = TRAFFIC.get((w.name, tiling))
+    e = TRAFFIC.get((w.name, tiling, B))
     if e is None:
         return None
     with open(kernel_source(w.shape), "rb") as f:
@@ -352,7 +354,7 @@ def main():
                    "params": w.shape.weight_count(), "flop_per_position": flop_pos},
         "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_bytes(w, tiling) if B == w.batch else None, "traffic_unit": "bytes per launch"},
+                     "traffic": traffic_bytes(w, tiling, B), "traffic_unit": "bytes per launch"},
         "latency_us": {"p10": float(np.percentile(lat, 10)), "p50": float(np.percentile(lat, 50)),
                        "p90": float(np.percentile(lat, 90)), "calls": int(lat.size)},
         "graph_replay_us": graph_us,

@@ -78,8 +78,6 @@ struct AzDevNet {
 #define AZ_DEP_POOL_OPAD 128
 #define AZ_DEP_ACTION_SLOTS 2048
 #define AZ_DEP_MAX_IN_PLANES 64
-// Largest batch for which the deployed network runs four waves per board by default
-#define AZ_DEP_SMALL_MAX_BATCH 256
 
 // Returns hipSuccess or the launch error.  tiling: 1 = large, 2 = small, 3 = medium.
 hipError_t az_launch_mfma(int dtype, int tiling, const AzDevNet& net, const float* planes,

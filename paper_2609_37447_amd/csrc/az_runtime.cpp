@@ -36,6 +36,7 @@ struct az_net {
   int dtype;
   int device;
   int tiling;  // 0 = chosen per batch
+  int cus;     // compute units of the device
   void* dmem;
   size_t dbytes;
   AzDevNet dn;
@@ -346,12 +347,22 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // for bf16 and fp8, and the two-board medium tiling (two workgroups per compute
 // unit) ties with it for int8.
 //
-// Deployed network: four waves per board while the batch leaves compute units
-// idle (up to one board per compute unit), one wave per board beyond.
+// Deployed network: the tiling with the shorter estimated time, rounds x time
+// per round.  A round is one board per compute unit with four waves per board,
+// and four (int8) or three (bf16, LDS-bound) boards per compute unit with one
+// wave per board; a round of the latter takes 2.26x (int8) or 2.56x (bf16) as
+// long as one of the former (14x160 on MI355X).
+int choose_dep_tiling(const az_net* n, int B) {
+  const bool i8 = n->dtype == AZ_INT8;
+  const long per1 = (long)n->cus * (i8 ? 4 : 3), per2 = n->cus;
+  const long r1 = (B + per1 - 1) / per1, r2 = (B + per2 - 1) / per2;
+  return r2 * 100 < r1 * (i8 ? 226 : 256) ? 2 : 1;
+}
+
 int choose_tiling(const az_net* n, int B) {
   if (n->dtype == AZ_F32) return 0;
   if (n->tiling) return n->tiling;
-  if (is_deployed(n->spec)) return B <= AZ_DEP_SMALL_MAX_BATCH ? 2 : 1;
+  if (is_deployed(n->spec)) return choose_dep_tiling(n, B);
   const int F = n->spec.filters;
   if (B < 512) return 2;
   if (n->dtype == AZ_BF16) return B >= 1024 ? 1 : 2;
@@ -587,9 +598,11 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   size_t total = 0;
   for (auto& sc : secs) { sc.off = total; total += align256(sc.bytes); }
 
-  int dev = 0;
+  int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
   void* dmem = nullptr;
   e = hipMalloc(&dmem, total);
   if (e != hipSuccess) { (void)hipGetLastError(); return hip_fail(e, "hipMalloc of the weights"); }
@@ -606,6 +619,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   net->dtype = dtype;
   net->device = dev;
   net->tiling = 0;
+  net->cus = cus > 0 ? cus : 1;
   net->dmem = dmem;
   net->dbytes = total;
   AzDevNet& d = net->dn;

@@ -208,20 +208,27 @@ def test_deployed_rows_do_not_depend_on_the_batch():
 
 
 def test_deployed_tiling_choice():
-    # four waves per board up to 256 boards (one per compute unit), one wave beyond
+    # the tiling with fewer rounds x time per round on 256 compute units: four
+    # waves per board (256 boards a round) against one wave per board (1,024 int8
+    # or 768 bf16 boards a round, 2.26x / 2.56x as long)
     import paper_2609_37447_amd as az
     shape = _shape(2)
     blob = azgen.make_weights(shape, 1036, alpha_fold=True, bf16=True)
-    net = az.az_net_load(az.spec_from_shape(shape, 1024), blob, "bf16")
-    try:
-        assert [az.az_net_tiling_for(net, B) for B in (1, 64, 256, 257, 1024)] == [2, 2, 2, 1, 1]
-        for t in (0, 1, 2):
-            assert az.az_net_set_tiling(net, t) == az.AZ_OK
-        assert az.az_net_tiling_for(net, 1024) == 2
-        for t in (3, -1):
-            assert az.az_net_set_tiling(net, t, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
-    finally:
-        az.az_net_free(net)
+    ws, acs = _scales(shape, blob)
+    want = {"int8": {1: 2, 64: 2, 256: 2, 512: 2, 513: 1, 768: 1, 1024: 1},
+            "bf16": {1: 2, 64: 2, 512: 2, 513: 1, 768: 1, 769: 2, 1024: 2}}
+    for dtype, cases in want.items():
+        net = az.az_net_load(az.spec_from_shape(shape, 1024), blob, dtype,
+                             *((ws, acs) if dtype == "int8" else (None, None)))
+        try:
+            assert {B: az.az_net_tiling_for(net, B) for B in cases} == cases
+            for t in (0, 1, 2):
+                assert az.az_net_set_tiling(net, t) == az.AZ_OK
+            assert az.az_net_tiling_for(net, 64) == 2
+            for t in (3, -1):
+                assert az.az_net_set_tiling(net, t, raise_on_error=False) == az.AZ_ERR_INVALID_ARG
+        finally:
+            az.az_net_free(net)
 
 
 def test_deployed_validate_gate():
