@@ -142,6 +142,10 @@ struct DepCfg {
   static constexpr int HEAD_END = OFF_O + 32 * 4;
   static constexpr int OFF_HC = (cmax(cmax(TOWER_END, X_END), HEAD_END) + 15) & ~15;  // head constants
   static constexpr int SMEM = OFF_HC + (2 * AZ_DEP_EMB_ROWS + 2 * DD) * 4;
+  // four-wave tiling: operand fragments shared by the heads' waves (four planes of
+  // 16 KB), past the one-wave layout
+  static constexpr int OFF_Q4 = (SMEM + 255) & ~255;
+  static constexpr int SMEM4 = OFF_Q4 + 4 * 16384;
   static_assert(OFF_T >= 64 * 128, "stem input fits in the T buffer");
   static constexpr int CPT = DF / T::KS;              // K steps per tap
   static constexpr int S = 9 * CPT;                   // K steps per layer
@@ -156,6 +160,58 @@ struct DepCfg {
 // output h is in LDS (int8: codes in H; bf16: hi parts in H, lo parts in X):
 // embedding, tokens, query-key logits and promotion offsets, legal-action
 // softmax, WDL value head.
+// WDL value head of one board, one wave (lane = 0..63), from the value
+// features U[c][sq] in LDS: y = relu(W1 u + b1), z = W2 y + b2, softmax over
+// (win, draw, loss), value = W - L.
+__device__ __forceinline__ void dep_wdl(const AzDevNet& p, const float* U, float* __restrict__ value,
+                                        float* __restrict__ wdl, int b, int lane) {
+  {
+    const int H = p.value_hidden, NU = p.value_channels * 64;
+    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
+    for (int k0 = 0; k0 < H; k0 += 64) {
+      const int k = k0 + lane;
+      const bool ok = k < H;
+      const int kk = ok ? k : 0;
+      float y = p.wdl_fc1_b[kk];
+      // fc1 row of unit kk in chunks of 16 inputs, the next chunk in flight
+      // (NU is a multiple of 64)
+      float wa[16], wb[16];
+      auto ld = [&](float(&d)[16], int i0) {
+#pragma unroll
+        for (int t = 0; t < 16; ++t) d[t] = p.wdl_fc1_t[(size_t)(i0 + t) * H + kk];
+      };
+      ld(wa, 0);
+      for (int i0 = 0; i0 < NU; i0 += 32) {
+        ld(wb, i0 + 16);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wa[t], U[i0 + t], y);
+        if (i0 + 32 < NU) ld(wa, i0 + 32);
+#pragma unroll
+        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wb[t], U[i0 + 16 + t], y);
+      }
+      y = ok ? fmaxf(y, 0.0f) : 0.0f;
+      z0 = __builtin_fmaf(p.wdl_fc2_w[kk], y, z0);
+      z1 = __builtin_fmaf(p.wdl_fc2_w[H + kk], y, z1);
+      z2 = __builtin_fmaf(p.wdl_fc2_w[2 * H + kk], y, z2);
+    }
+    z0 = wave_sum(z0) + p.wdl_fc2_b[0];
+    z1 = wave_sum(z1) + p.wdl_fc2_b[1];
+    z2 = wave_sum(z2) + p.wdl_fc2_b[2];
+    const float m = fmaxf(z0, fmaxf(z1, z2));
+    const float e0 = expf(z0 - m), e1 = expf(z1 - m), e2 = expf(z2 - m);
+    const float is = 1.0f / (e0 + e1 + e2);
+    if (lane == 0) {
+      const float pw = e0 * is, pd = e1 * is, pl = e2 * is;
+      value[b] = pw - pl;
+      if (wdl) {
+        wdl[3 * (size_t)b + 0] = pw;
+        wdl[3 * (size_t)b + 1] = pd;
+        wdl[3 * (size_t)b + 2] = pl;
+      }
+    }
+  }
+}
+
 template <int MK>
 __device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, const uint8_t* __restrict__ legal,
                                           float* __restrict__ policy, float* __restrict__ value,
@@ -428,53 +484,318 @@ __device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, cons
     }
   }
 
-  // ---- WDL head: y = relu(W1 u + b1), z = W2 y + b2, softmax, value = W - L
+  // ---- WDL head
+  dep_wdl(p, reinterpret_cast<const float*>(smem + C::OFF_U), value, wdl, b, lane);
+}
+
+// Heads of one board shared by the four waves of az_dep_kernel4 (wave = 0..3,
+// lane = 0..63), once the final tower output h is in LDS.  The arithmetic is
+// dep_heads' operation for operation: every accumulator tile runs the same
+// chain of products, split operands are split the same way, and the softmax
+// normaliser is summed in the same order, so the outputs are bitwise the same.
+// The work is spread as the tower's is: wave w owns token / query / key block w
+// and one 32x32 tile of the logits S; operands that cross waves go through LDS
+// as the very fragments a single wave would have taken from its registers
+// (fragment set [square block][K step][lane] of 16 bytes).
+template <int MK>
+__device__ __forceinline__ void dep_heads4(const AzDevNet& p, uint8_t* smem, const uint8_t* __restrict__ legal,
+                                           float* __restrict__ policy, float* __restrict__ value,
+                                           float* __restrict__ wdl, int b, int wave, int lane) {
+  using C = DepCfg<MK>;
+  using R = Rot<C::RB>;
+  using RX = Rot<C::RBX>;
+  constexpr bool QUANT = C::QUANT;
+  constexpr int RB = C::RB, OFF_H = C::OFF_H;
+  constexpr int FS = 64 * 16;                   // bytes of one fragment set
+  static_assert(DTB == 4, "one token block per wave");
+  const int l32 = lane & 31, lhi = lane >> 5;
+  const float* HC = reinterpret_cast<const float*>(smem + C::OFF_HC);
+  uint8_t* const q4 = smem + C::OFF_Q4;
+  // fragment set of K step s (0..7) of square block n in one of the four 16 KB planes
+  auto fset = [&](int plane, int n, int s) { return q4 + plane * 16384 + ((n * 8 + s) * 64 + lane) * 16; };
+
+  // action table entries and legal-mask words of this wave's two groups of 256
+  // actions (actions 256 i + 4 lane .. + 3), in flight during the products
+  constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256, GW = NIT / 4;
+  static_assert(NIT % 4 == 0, "action groups per wave");
+  uint4 tbl[GW];
+  uint32_t mkw[GW];
   {
-    const float* U = reinterpret_cast<const float*>(smem + C::OFF_U);
-    const int H = p.value_hidden, NU = p.value_channels * 64;
-    float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f;
-    for (int k0 = 0; k0 < H; k0 += 64) {
-      const int k = k0 + lane;
-      const bool ok = k < H;
-      const int kk = ok ? k : 0;
-      float y = p.wdl_fc1_b[kk];
-      // fc1 row of unit kk in chunks of 16 inputs, the next chunk in flight
-      // (NU is a multiple of 64)
-      float wa[16], wb[16];
-      auto ld = [&](float(&d)[16], int i0) {
+    const uint8_t* lg = legal + (size_t)b * NA;
 #pragma unroll
-        for (int t = 0; t < 16; ++t) d[t] = p.wdl_fc1_t[(size_t)(i0 + t) * H + kk];
-      };
-      ld(wa, 0);
-      for (int i0 = 0; i0 < NU; i0 += 32) {
-        ld(wb, i0 + 16);
-#pragma unroll
-        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wa[t], U[i0 + t], y);
-        if (i0 + 32 < NU) ld(wa, i0 + 32);
-#pragma unroll
-        for (int t = 0; t < 16; ++t) y = __builtin_fmaf(wb[t], U[i0 + 16 + t], y);
-      }
-      y = ok ? fmaxf(y, 0.0f) : 0.0f;
-      z0 = __builtin_fmaf(p.wdl_fc2_w[kk], y, z0);
-      z1 = __builtin_fmaf(p.wdl_fc2_w[H + kk], y, z1);
-      z2 = __builtin_fmaf(p.wdl_fc2_w[2 * H + kk], y, z2);
+    for (int g = 0; g < GW; ++g) {
+      const int a0 = 256 * (wave * GW + g) + 4 * lane;
+      const bool in = a0 < NA;
+      tbl[g] = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
+      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
+      mkw[g] = in ? mk0 : 0u;
     }
-    z0 = wave_sum(z0) + p.wdl_fc2_b[0];
-    z1 = wave_sum(z1) + p.wdl_fc2_b[1];
-    z2 = wave_sum(z2) + p.wdl_fc2_b[2];
-    const float m = fmaxf(z0, fmaxf(z1, z2));
-    const float e0 = expf(z0 - m), e1 = expf(z1 - m), e2 = expf(z2 - m);
-    const float is = 1.0f / (e0 + e1 + e2);
-    if (lane == 0) {
-      const float pw = e0 * is, pd = e1 * is, pl = e2 * is;
-      value[b] = pw - pl;
-      if (wdl) {
-        wdl[3 * (size_t)b + 0] = pw;
-        wdl[3 * (size_t)b + 1] = pd;
-        wdl[3 * (size_t)b + 2] = pl;
+  }
+
+  // every weight fragment of the wave's embedding rows and query / key rows,
+  // issued at once: the heads then wait for one load latency, not one per step
+  constexpr int ES = DF / 16, QS = DD / 16;
+  bf16x8 awe[ES][2], aq[QS], ak[QS];
+  {
+    const uint8_t* ew = static_cast<const uint8_t*>(p.emb_w) + (size_t)lane * 16;
+    const uint8_t* qp = static_cast<const uint8_t*>(p.q_w) + (size_t)lane * 16;
+    const uint8_t* kp = static_cast<const uint8_t*>(p.k_w) + (size_t)lane * 16;
+#pragma unroll
+    for (int st = 0; st < ES; ++st) {
+      awe[st][0] = g_frag<MK_BF16>(ew + (st * DEMB + wave) * FS);
+      awe[st][1] = g_frag<MK_BF16>(ew + (st * DEMB + DTB) * FS);
+    }
+#pragma unroll
+    for (int st = 0; st < QS; ++st) {
+      aq[st] = g_frag<MK_BF16>(qp + (st * DTB + wave) * FS);
+      ak[st] = g_frag<MK_BF16>(kp + (st * DTB + wave) * FS);
+    }
+  }
+
+  // ---- embedding: token rows of block wave (both square blocks) and the value
+  // rows on square block wave & 1 (kept by waves 0 and 1)
+  const int nv = wave & 1;
+  f32x16 tk[2], ua;
+  {
+#pragma unroll
+    for (int s = 0; s < ES; ++s) {
+      const bf16x8(&aw)[2] = awe[s];
+      bf16x8 bx[2], bh[2];
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int j = n * 32 + l32;
+        if constexpr (QUANT) {
+          const uint2 v = *reinterpret_cast<const uint2*>(smem + OFF_H + j * RB + (R::pos(s, R::sw(j)) << 4) + 8 * lhi);
+          bx[n] = __builtin_bit_cast(
+              bf16x8, make_uint4(pack_bf16x2(code_value<MK, 0>(v.x), code_value<MK, 1>(v.x)),
+                                 pack_bf16x2(code_value<MK, 2>(v.x), code_value<MK, 3>(v.x)),
+                                 pack_bf16x2(code_value<MK, 0>(v.y), code_value<MK, 1>(v.y)),
+                                 pack_bf16x2(code_value<MK, 2>(v.y), code_value<MK, 3>(v.y))));
+        } else {
+          bx[n] = *reinterpret_cast<const bf16x8*>(smem + C::OFF_X + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+          bh[n] = *reinterpret_cast<const bf16x8*>(smem + OFF_H + j * C::RBX + (RX::pos(2 * s + lhi, RX::sw(j)) << 4));
+        }
+      }
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        tk[n] = mma_bf16(aw[0], bx[n], s == 0 ? f32x16{} : tk[n]);
+        if constexpr (!QUANT) tk[n] = mma_bf16(aw[0], bh[n], tk[n]);
+      }
+      const bf16x8 bxv = nv ? bx[1] : bx[0];
+      ua = mma_bf16(aw[1], bxv, s == 0 ? f32x16{} : ua);
+      if constexpr (!QUANT) {
+        const bf16x8 bhv = nv ? bh[1] : bh[0];
+        ua = mma_bf16(aw[1], bhv, ua);
       }
     }
   }
+  wave_lds_sync();  // H and X are dead from here on
+
+  // token values relu(acc * scale + bias), as the query / key products' B
+  // fragments of K steps 2 wave and 2 wave + 1; value features u[c][sq] to LDS
+  {
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      const int r0 = 32 * wave + 8 * jq + 4 * lhi;
+      const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+      const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
+      const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
+#pragma unroll
+      for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) tk[n][4 * jq + r] = fmaxf(__builtin_fmaf(tk[n][4 * jq + r], sv[r], bv[r]), 0.0f);
+    }
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float x[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) x[t] = tk[n][8 * h + t];
+        bf16x8 hi, lo;
+        split8(x, hi, lo);
+        *reinterpret_cast<bf16x8*>(fset(0, n, 2 * wave + h)) = hi;
+        *reinterpret_cast<bf16x8*>(fset(1, n, 2 * wave + h)) = lo;
+      }
+    if (wave < 2) {
+      float* U = reinterpret_cast<float*>(smem + C::OFF_U);
+      const int V = p.value_channels;
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int r0 = DD + 8 * jq + 4 * lhi;
+        const float4 sc = *reinterpret_cast<const float4*>(HC + r0);
+        const float4 bc = *reinterpret_cast<const float4*>(HC + AZ_DEP_EMB_ROWS + r0);
+        const float sv[4] = {sc.x, sc.y, sc.z, sc.w}, bv[4] = {bc.x, bc.y, bc.z, bc.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ch = 8 * jq + 4 * lhi + r;
+          if (ch < V) {
+            float u = __builtin_fmaf(ua[4 * jq + r], sv[r], bv[r]);
+            if (p.value_conv_relu) u = fmaxf(u, 0.0f);
+            U[ch * 64 + nv * 32 + l32] = u;
+          }
+        }
+      }
+    }
+  }
+  wave_lds_sync();
+
+  // query and key block wave: Q^T = Wq tok^T + bq, K^T = Wk tok^T + bk over the
+  // eight token K steps (hi, then lo)
+  f32x16 Qa[2], Ka[2];
+  {
+#pragma unroll
+    for (int s = 0; s < QS; ++s) {
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const bf16x8 xh = *reinterpret_cast<const bf16x8*>(fset(0, n, s));
+        const bf16x8 xl = *reinterpret_cast<const bf16x8*>(fset(1, n, s));
+        Qa[n] = mma_bf16(aq[s], xh, s == 0 ? f32x16{} : Qa[n]);
+        Qa[n] = mma_bf16(aq[s], xl, Qa[n]);
+        Ka[n] = mma_bf16(ak[s], xh, s == 0 ? f32x16{} : Ka[n]);
+        Ka[n] = mma_bf16(ak[s], xl, Ka[n]);
+      }
+    }
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      const int r0 = 32 * wave + 8 * jq + 4 * lhi;
+      const float4 bq = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + r0);
+      const float4 bk = *reinterpret_cast<const float4*>(HC + 2 * AZ_DEP_EMB_ROWS + DD + r0);
+      const float qv[4] = {bq.x, bq.y, bq.z, bq.w}, kv[4] = {bk.x, bk.y, bk.z, bk.w};
+#pragma unroll
+      for (int n = 0; n < 2; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          Qa[n][4 * jq + r] += qv[r];
+          Ka[n][4 * jq + r] += kv[r];
+        }
+    }
+  }
+  wave_lds_sync();  // token fragments dead
+  // the logits' A (query) and B (key) fragments of K steps 2 wave, 2 wave + 1
+#pragma unroll
+  for (int n = 0; n < 2; ++n)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float x[8], y[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        x[t] = Qa[n][8 * h + t];
+        y[t] = Ka[n][8 * h + t];
+      }
+      bf16x8 qh, ql, kh, kl;
+      split8(x, qh, ql);
+      split8(y, kh, kl);
+      *reinterpret_cast<bf16x8*>(fset(0, n, 2 * wave + h)) = qh;
+      *reinterpret_cast<bf16x8*>(fset(1, n, 2 * wave + h)) = ql;
+      *reinterpret_cast<bf16x8*>(fset(2, n, 2 * wave + h)) = kh;
+      *reinterpret_cast<bf16x8*>(fset(3, n, 2 * wave + h)) = kl;
+    }
+  wave_lds_sync();
+
+  // S tile (mf, nt) = (wave >> 1, wave & 1): S[f][t] = sum_d Q[f][d] K[t][d]
+  // (hi*hi + hi*lo + lo*hi); the promotion offsets O^T = Wp K^T of the last row's
+  // destinations (square block 1, written by wave 3)
+  {
+    const int mf = wave >> 1, nt = wave & 1;
+    const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
+    bf16x8 apw[DD / 16];
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) apw[s] = g_frag<MK_BF16>(pw + s * FS);
+    f32x16 Sa, Oa;
+#pragma unroll
+    for (int s = 0; s < DD / 16; ++s) {
+      const bf16x8 qh = *reinterpret_cast<const bf16x8*>(fset(0, mf, s));
+      const bf16x8 ql = *reinterpret_cast<const bf16x8*>(fset(1, mf, s));
+      const bf16x8 kh = *reinterpret_cast<const bf16x8*>(fset(2, nt, s));
+      const bf16x8 kl = *reinterpret_cast<const bf16x8*>(fset(3, nt, s));
+      Sa = mma_bf16(qh, kh, s == 0 ? f32x16{} : Sa);
+      Sa = mma_bf16(qh, kl, Sa);
+      Sa = mma_bf16(ql, kh, Sa);
+      Oa = mma_bf16(apw[s], kh, s == 0 ? f32x16{} : Oa);
+      Oa = mma_bf16(apw[s], kl, Oa);
+    }
+    // logits pre-scaled by log2(e) for the exp2 softmax
+    const float log2e = 1.4426950408889634f;
+    const float ss = log2e / sqrtf((float)DD);
+    float* S = reinterpret_cast<float*>(smem + C::OFF_S);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int f = 32 * mf + 8 * (v / 4) + 4 * lhi + v % 4, t = 32 * nt + l32;
+      S[f * 64 + t] = Sa[v] * ss;
+    }
+    float* O = reinterpret_cast<float*>(smem + C::OFF_O);
+    if (wave == 3 && lhi == 0 && l32 >= 24) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) O[(l32 - 24) * 4 + k] = Oa[k] * log2e;
+    }
+  }
+  wave_lds_sync();  // query / key fragments dead
+
+  // ---- legal-action softmax: wave w gathers and exponentiates groups 2w, 2w + 1;
+  // the maximum is exact in any order, the normaliser is summed by wave 0 over all
+  // groups in the one-wave order
+  float* E = reinterpret_cast<float*>(q4);            // numerators, 2048 slots
+  float* MX = reinterpret_cast<float*>(q4 + 8192);    // per-wave maxima, then 1 / sum
+  {
+    const float* S = reinterpret_cast<const float*>(smem + C::OFF_S);
+    const float* O = reinterpret_cast<const float*>(smem + C::OFF_O);
+    float e[GW][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int g = 0; g < GW; ++g) {
+      const int a0 = 256 * (wave * GW + g) + 4 * lane;
+      const bool in = a0 < NA;  // NA is a multiple of 4
+      const uint4 tb = tbl[g];
+      const uint32_t mk = mkw[g];
+      const uint32_t te[4] = {tb.x, tb.y, tb.z, tb.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t x = te[r], pr = x >> 12;
+        const float z = S[x & 4095u] + (pr ? O[pr - 1] : 0.0f);
+        const bool ok = in && ((mk >> (8 * r)) & 0xffu);
+        e[g][r] = ok ? z : -INFINITY;
+        mx = fmaxf(mx, e[g][r]);
+      }
+    }
+    mx = wave_max(mx);
+    if (lane == 0) MX[wave] = mx;
+    wave_lds_sync();
+    mx = fmaxf(fmaxf(MX[0], MX[1]), fmaxf(MX[2], MX[3]));
+    const float msub = mx == -INFINITY ? 0.0f : mx;
+#pragma unroll
+    for (int g = 0; g < GW; ++g) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) e[g][r] = __builtin_amdgcn_exp2f(e[g][r] - msub);  // exp2(-inf) = 0
+      *reinterpret_cast<float4*>(E + 256 * (wave * GW + g) + 4 * lane) = make_float4(e[g][0], e[g][1], e[g][2], e[g][3]);
+    }
+    wave_lds_sync();
+    if (wave == 0) {
+      float sum = 0.0f;
+#pragma unroll
+      for (int i = 0; i < NIT; ++i) {
+        const float4 v = *reinterpret_cast<const float4*>(E + 256 * i + 4 * lane);
+        sum += v.x;
+        sum += v.y;
+        sum += v.z;
+        sum += v.w;
+      }
+      sum = wave_sum(sum);
+      if (lane == 0) MX[4] = sum > 0.0f ? 1.0f / sum : 0.0f;
+    }
+    wave_lds_sync();
+    const float inv = MX[4];
+    float* pol = policy + (size_t)b * NA;
+#pragma unroll
+    for (int g = 0; g < GW; ++g) {
+      const int a0 = 256 * (wave * GW + g) + 4 * lane;
+      if (a0 < NA)
+        *reinterpret_cast<float4*>(pol + a0) = make_float4(e[g][0] * inv, e[g][1] * inv, e[g][2] * inv, e[g][3] * inv);
+    }
+  }
+
+  // ---- WDL head (wave 1): y = relu(W1 u + b1), z = W2 y + b2, softmax, value = W - L
+  if (wave == 1) dep_wdl(p, reinterpret_cast<const float*>(smem + C::OFF_U), value, wdl, b, lane);
 }
 
 template <int MK>
@@ -1009,7 +1330,7 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
   constexpr bool QUANT = C::QUANT;
   constexpr int RB = C::RB, OFF_H = C::OFF_H, OFF_T = C::OFF_T, OFF_Z = C::OFF_Z;
 
-  __shared__ __attribute__((aligned(16))) uint8_t smem[C::SMEM];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[C::SMEM4];
 
   // Tiles of a layer: five 32-channel blocks x two half-board square blocks.
   // Wave w (one per SIMD) owns both tiles of block w, and waves 0 and 1 also
@@ -1541,8 +1862,8 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
   else if (wave == 1) trunk(std::integral_constant<int, 1>{});
   else trunk(std::integral_constant<int, -1>{});
   __syncthreads();
-  // ---- heads: wave 0
-  if (wave == 0) dep_heads<MK>(p, smem, legal, policy, value, wdl, b, lane);
+  // ---- heads, shared by the four waves
+  dep_heads4<MK>(p, smem, legal, policy, value, wdl, b, wave, lane);
 }
 
 
