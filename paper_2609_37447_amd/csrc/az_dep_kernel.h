@@ -1559,6 +1559,16 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         // the next layer's epilogue constants, in flight during this layer
         float4 kn[KPL];
         if (has_next) load_consts(n_conv + 2, kn);
+        // a pooling layer's projection weights (waves 0 and 1: output 64 wave +
+        // lane, all 2g inputs as [i/4] float4s), in flight during the K loop
+        constexpr int NWP = POOL ? 2 * DG / 4 : 1;
+        float4 wpool[NWP];
+        if constexpr (POOL) {
+          const float4* wt = reinterpret_cast<const float4*>(p.pool_wt) +
+                             (size_t)(n_conv / 2 / p.pool_every) * (2 * DG / 4) * AZ_DEP_POOL_OPAD + 64 * (wave & 1) + lane;
+#pragma unroll
+          for (int i4 = 0; i4 < NWP; ++i4) wpool[i4] = wt[(size_t)i4 * AZ_DEP_POOL_OPAD];
+        }
         // B fragments of one K step.  Channel step cs reads logical chunk
         // lc = 2 cs + lhi of the tap's row, at chunk position (lc + rot) mod NC with
         // rot the row's rotation: from a per-tap base b0 = row + 16 (lhi + rot) the
@@ -1679,52 +1689,40 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
             }
           });
           wave_lds_sync();
-          // (2) wave 0, lane pc < g: board sum (fp64) and maximum of its row;
-          //     g = [mean, max]
+          // (2) wave w, lane l < g/4: board sum (fp64) and maximum of row
+          //     pc = g/4 w + l; g = [mean, max]
           double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
-          if (wave == 0 && lane < DG) {
+          static_assert(DG % 4 == 0, "pooled rows per wave");
+          if (lane < DG / 4) {
+            const int pc = (DG / 4) * wave + lane;
             double sum = 0.0;
             float mx = 0.0f;  // activations are >= 0
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-              const float4 v = *reinterpret_cast<const float4*>(pt + lane * 64 + ((j ^ (lane & 15)) << 2));
+              const float4 v = *reinterpret_cast<const float4*>(pt + pc * 64 + ((j ^ (pc & 15)) << 2));
               sum += (double)v.x;
               sum += (double)v.y;
               sum += (double)v.z;
               sum += (double)v.w;
               mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
             }
-            pg[lane] = sum * (1.0 / 64.0);
-            pg[DG + lane] = (double)mx;
+            pg[pc] = sum * (1.0 / 64.0);
+            pg[DG + pc] = (double)mx;
           }
           wave_lds_sync();
           // (3) c[o] = sum_i Wg[o][i] g[i] in fp64 (fp32 weights are exact): waves 0
-          //     and 1 take output 64 wave + lane; the weights, [i/4][o][4] floats,
-          //     stream in chunks of 16 inputs with the next chunk in flight
+          //     and 1 take output 64 wave + lane with the prefetched weights
           if (wave < 2) {
             const int o = 64 * wave + lane;
-            const float4* wt = reinterpret_cast<const float4*>(p.pool_wt) +
-                               (size_t)(n_conv / 2 / p.pool_every) * (2 * DG / 4) * AZ_DEP_POOL_OPAD + o;
-            constexpr int NCH = 2 * DG / 16;
-            float4 wbuf[2][4];
-            auto load_chunk = [&](float4(&dst)[4], int chk) {
-#pragma unroll
-              for (int k4 = 0; k4 < 4; ++k4) dst[k4] = wt[(size_t)(4 * chk + k4) * AZ_DEP_POOL_OPAD];
-            };
-            load_chunk(wbuf[0], 0);
             double co = 0.0;
 #pragma unroll
-            for (int chk = 0; chk < NCH; ++chk) {
-              if (chk + 1 < NCH) load_chunk(wbuf[(chk + 1) & 1], chk + 1);
-#pragma unroll
-              for (int k4 = 0; k4 < 4; ++k4) {
-                const float4 w = wbuf[chk & 1][k4];
-                const double* gi = pg + 16 * chk + 4 * k4;
-                co = __builtin_fma((double)w.x, gi[0], co);
-                co = __builtin_fma((double)w.y, gi[1], co);
-                co = __builtin_fma((double)w.z, gi[2], co);
-                co = __builtin_fma((double)w.w, gi[3], co);
-              }
+            for (int i4 = 0; i4 < NWP; ++i4) {
+              const float4 w = wpool[i4];
+              const double* gi = pg + 4 * i4;
+              co = __builtin_fma((double)w.x, gi[0], co);
+              co = __builtin_fma((double)w.y, gi[1], co);
+              co = __builtin_fma((double)w.z, gi[2], co);
+              co = __builtin_fma((double)w.w, gi[3], co);
             }
             if (o < DFR) reinterpret_cast<float*>(smem + C::OFF_C)[o] = (float)co;
           }
