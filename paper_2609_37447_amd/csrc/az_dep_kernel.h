@@ -1429,7 +1429,6 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
     load_consts(1, k0);
     store_consts(0, k0);
   }
-  __syncthreads();
 
   // ---- stem and tower of one wave.  XN >= 0: the wave also owns tile (4, XN).
   // Fragment / accumulator set m < MBW is block mb0 + m (both tiles); set MBW,
@@ -1462,8 +1461,9 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
       const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)lane * 16;
       f32x16 sacc[NAF][NBW];
       // 36 K steps (tap = st / 4, 16 channels each): A fragments of step st in ring
-      // slot st % 4, loaded three steps ahead; B fragments one step ahead
-      constexpr int SR = 4, NST = 9 * DCP / 16;
+      // slot st % 12, loaded eleven steps ahead, the first ones before the ingest
+      // barrier; B fragments one step ahead
+      constexpr int SR = 12, NST = 9 * DCP / 16;
       bf16x8 a[SR][NAF];
       auto load_a = [&](int st) {
 #pragma unroll
@@ -1482,6 +1482,7 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
       };
 #pragma unroll
       for (int st = 0; st < SR - 1; ++st) load_a(st);
+      __syncthreads();  // the ingest's planes and constants are in LDS
       bf16x8 bcur[NBW], bnext[NBW];
       load_b(0, bcur);
 #pragma unroll
