@@ -51,10 +51,10 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {  # (workload, tiling, batch): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
     ("net20x128_int8_b1024", 3, 1024): ("faf2c3970238b8113f568cabf1e9363b742d350fdec26bd0ffc19cbf57c667f6",
                                         33413.4, 18704.0),
-    ("deployed14x160_int8_b1024", 1, 1024): ("0492418980244a44ad54fdece8376f64984a685d3a1d41e624a5846f823d4940",
-                                             46066.0, 29226.5),
-    ("deployed14x160_int8_b1024", 2, 64): ("0492418980244a44ad54fdece8376f64984a685d3a1d41e624a5846f823d4940",
-                                           29836.8, 1736.0),
+    ("deployed14x160_int8_b1024", 1, 1024): ("68cdf225840b036ee0f75ce815c89e8a98ac5cf960f2dc74dbe4a2f2f29029d3",
+                                             46253.9, 30140.0),
+    ("deployed14x160_int8_b1024", 2, 64): ("68cdf225840b036ee0f75ce815c89e8a98ac5cf960f2dc74dbe4a2f2f29029d3",
+                                           29236.0, 472.0),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.

@@ -11,8 +11,8 @@
 // layer, so global pooling, the heads and both softmaxes need no exchange with
 // other waves.  az_dep_kernel4 (small batches, where the batch offers about a
 // board per compute unit): four waves, one per SIMD, share a layer's ten 32x32
-// tiles, three at most per SIMD, and meet at a barrier per layer; the heads
-// run in one of them.
+// tiles, three at most per SIMD, and meet at a barrier per layer; they share
+// the heads as well, exchanging operand fragments through LDS.
 //
 // Tower.  Every 3x3 convolution is an implicit GEMM D[ch][sq] = sum_k
 // W[ch][k] X[k][sq], k = tap * C + c, with weights as the A operand (streamed
@@ -26,10 +26,10 @@
 //
 // Global pooling (every pool_every-th block).  After the first convolution's
 // K loop, the pooled channels (the last F/4) are activated from the
-// accumulators, their board sum (fp64) and maximum are reduced across the 32
-// lanes of each half-wave, and the projection c = Wg [mean, max] runs in fp64
-// over the wave; c (rounded to fp32) is then added to the regular channels in
-// the same epilogue that writes them.
+// accumulators and transposed through LDS; one lane per pooled channel reduces
+// its board sum (fp64) and maximum, and the projection c = Wg [mean, max] runs
+// in fp64, one or two outputs per lane; c (rounded to fp32) is then added to
+// the regular channels in the same epilogue that writes them.
 //
 // bf16 networks carry the residual stream h as hi + lo: hi = bf16(h) is the
 // convolution operand in LDS, lo = bf16(h - hi) stays in the registers of the
@@ -41,9 +41,11 @@
 // each accumulator tile is split into bf16 hi + lo parts and used directly as
 // an MFMA operand, with the next weight matrix packed in the order the
 // accumulator registers hold their rows (a permutation of the K dimension
-// applied to both operands of the product).  Query-key logits are written to
-// LDS once, gathered through the action table, and soft-maxed over the legal
-// actions in fp32; the WDL head runs on the vector ALUs.
+// applied to both operands of the product); with four waves per board the
+// tiles that cross waves go through LDS as those same fragments.  Query-key
+// logits are written to LDS once, gathered through the action table, and
+// soft-maxed over the legal actions in fp32; the WDL head runs on the vector
+// ALUs.
 #pragma once
 
 #include "az_internal.h"
@@ -149,17 +151,12 @@ struct DepCfg {
   static_assert(OFF_T >= 64 * 128, "stem input fits in the T buffer");
   static constexpr int CPT = DF / T::KS;              // K steps per tap
   static constexpr int S = 9 * CPT;                   // K steps per layer
-  static constexpr int NBUF = 3;                      // weight ring (steps), loaded NBUF-1 ahead
+  static constexpr int NBUF = 3;                      // one-wave weight ring (steps), loaded NBUF-1 ahead
   static_assert((2 * S) % NBUF == 0, "every block's first conv starts at ring slot 0");
   static constexpr int STEP_BYTES = DNMB * 64 * T::FB;
   static constexpr size_t LAYER_BYTES = (size_t)S * STEP_BYTES;
 };
 
-
-// Heads of one board, run by one wave (lane = 0..63) once the final tower
-// output h is in LDS (int8: codes in H; bf16: hi parts in H, lo parts in X):
-// embedding, tokens, query-key logits and promotion offsets, legal-action
-// softmax, WDL value head.
 // WDL value head of one board, one wave (lane = 0..63), from the value
 // features U[c][sq] in LDS: y = relu(W1 u + b1), z = W2 y + b2, softmax over
 // (win, draw, loss), value = W - L.
@@ -212,6 +209,10 @@ __device__ __forceinline__ void dep_wdl(const AzDevNet& p, const float* U, float
   }
 }
 
+// Heads of one board, run by one wave (lane = 0..63) once the final tower
+// output h is in LDS (int8: codes in H; bf16: hi parts in H, lo parts in X):
+// embedding, tokens, query-key logits and promotion offsets, legal-action
+// softmax, WDL value head.
 template <int MK>
 __device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, const uint8_t* __restrict__ legal,
                                           float* __restrict__ policy, float* __restrict__ value,
