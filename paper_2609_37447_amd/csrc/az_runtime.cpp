@@ -350,13 +350,14 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Deployed network: the tiling with the shorter estimated time, rounds x time
 // per round.  A round is one board per compute unit with four waves per board,
 // and four (int8) or three (bf16, LDS-bound) boards per compute unit with one
-// wave per board; a round of the latter takes 2.26x (int8) or 2.56x (bf16) as
-// long as one of the former (14x160 on MI355X).
+// wave per board; a round of the latter takes 2.5x (int8: ~370 against ~150 us)
+// or 2.8x (bf16: ~630 against ~225 us) as long as one of the former (14x160 on
+// MI355X).
 int choose_dep_tiling(const az_net* n, int B) {
   const bool i8 = n->dtype == AZ_INT8;
   const long per1 = (long)n->cus * (i8 ? 4 : 3), per2 = n->cus;
   const long r1 = (B + per1 - 1) / per1, r2 = (B + per2 - 1) / per2;
-  return r2 * 100 < r1 * (i8 ? 226 : 256) ? 2 : 1;
+  return r2 * 10 < r1 * (i8 ? 25 : 28) ? 2 : 1;
 }
 
 int choose_tiling(const az_net* n, int B) {

@@ -210,7 +210,7 @@ def test_deployed_rows_do_not_depend_on_the_batch():
 def test_deployed_tiling_choice():
     # the tiling with fewer rounds x time per round on 256 compute units: four
     # waves per board (256 boards a round) against one wave per board (1,024 int8
-    # or 768 bf16 boards a round, 2.26x / 2.56x as long)
+    # or 768 bf16 boards a round, 2.5x / 2.8x as long)
     import paper_2609_37447_amd as az
     shape = _shape(2)
     blob = azgen.make_weights(shape, 1036, alpha_fold=True, bf16=True)
