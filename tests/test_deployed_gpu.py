@@ -143,6 +143,23 @@ def test_deployed_no_pooling_and_other_shapes(tiling):
     _check(got, ref, legal, "bf16")
 
 
+@pytest.mark.parametrize("tiling", [1, 2])
+@pytest.mark.parametrize("pool_every,dtype", [(1, "int8"), (3, "bf16")])
+def test_deployed_pooling_period(pool_every, dtype, tiling):
+    # global pooling in every block, or in every third (blocks 2 and 5 of six)
+    shape = _shape(3 if pool_every == 1 else 6, pool_every=pool_every)
+    blob = azgen.make_weights(shape, 1066, alpha_fold=True, bf16=True)
+    planes, legal = _inputs(shape, 7, 2266 + pool_every)
+    if dtype == "int8":
+        ws, acs = _scales(shape, blob)
+        got = gpu_eval(shape, blob, "int8", planes, legal, ws, acs, tiling=tiling)
+        ref = OD.forward_quant(shape, blob, ws, acs, planes, legal)
+    else:
+        got = gpu_eval(shape, blob, "bf16", planes, legal, tiling=tiling)
+        ref = OD.forward(shape, blob, planes, legal)
+    _check(got, ref, legal, dtype)
+
+
 def test_deployed_14x160_int8_batch1024_sampled_rows():
     w = azgen.WORKLOADS["deployed14x160_int8_b1024"]
     blob = azgen.workload_weights(w)
