@@ -1435,12 +1435,17 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
   // Fragment / accumulator set m < MBW is block mb0 + m (both tiles); set MBW,
   // when present, is block 4 (tile XN only).  Every wave meets the same
   // sequence of workgroup barriers.
-  auto trunk = [&](auto xn_c) {
+  // int8 layers without pooling move the epilogue of tile (4, n) from wave n to
+  // wave 2 + n (MV = n), which finishes its K loop earlier; the tile's
+  // accumulators go through LDS.
+  constexpr bool MOVE = QUANT;
+  auto trunk = [&](auto xn_c, auto mv_c) {
     constexpr int XN = decltype(xn_c)::value;
+    constexpr int MV = decltype(mv_c)::value;      // tile (4, MV)'s moved epilogue (waves 2, 3)
     constexpr int NAF = MBW + (XN >= 0 ? 1 : 0);   // weight fragments per K step
     auto blk_of = [&](int m) { return m < MBW ? mb0 + m : DNMB - 1; };
-    auto n_lo = [](int m) constexpr { return m < MBW ? 0 : XN; };
-    auto n_hi = [](int m) constexpr { return m < MBW ? NBW : XN + 1; };
+    auto n_lo = [](int m) constexpr { return m < MBW ? 0 : (XN >= 0 ? XN : MV); };
+    auto n_hi = [](int m) constexpr { return m < MBW ? NBW : (XN >= 0 ? XN : MV) + 1; };
 
     // residual stream of the board (bf16 networks): h = hi + lo, hi = bf16(h) in
     // the H buffer (the convolution operand), lo = bf16(h - hi) packed here, two
@@ -1540,7 +1545,7 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
     // ---- residual tower
     {
       constexpr int CPT = C::CPT;
-      acc_t c[NAF][NBW];
+      acc_t c[MBW + 1][NBW];
       const int nconv = 2 * p.blocks;
 
       const int l32_ = l32, lhi_ = lhi;
@@ -1738,7 +1743,7 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
           hi = p.qhi[n_conv + 1];
           rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
         }
-        constexpr int NRUN = NAF * 4, EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
+        constexpr int EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
         constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
         constexpr bool RHI = !QUANT && SECOND;    // residual hi parts, read in place
         float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
@@ -1766,10 +1771,13 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
             for (int n = n_lo(m); n < n_hi(m); ++n) rhi[slot][n] = *reinterpret_cast<const uint2*>(smem + ep_addr(m, q, n));
           }
         };
-        static_for<0, EP_AHEAD>([&](auto k_c) { ep_load(k_c); });
-        static_for<0, NRUN>([&](auto k_c) {
+        // runs [K0, K1) (run k: set k / 4, channels 8 (k % 4) .. of the set's block)
+        auto epi_runs = [&](auto k0_c, auto k1_c) {
+        constexpr int K0 = decltype(k0_c)::value, K1 = decltype(k1_c)::value;
+        static_for<K0, (K0 + EP_AHEAD < K1 ? K0 + EP_AHEAD : K1)>([&](auto k_c) { ep_load(k_c); });
+        static_for<K0, K1>([&](auto k_c) {
           constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
-          if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
+          if constexpr (k + EP_AHEAD < K1) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
           const float4 bb = kb[slot];
 #pragma unroll
           for (int n = n_lo(m); n < n_hi(m); ++n) {
@@ -1827,6 +1835,25 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
             }
           }
         });
+        };
+        constexpr bool MOVED = MOVE && !POOL;   // this layer moves tile (4, n)'s epilogue
+        if constexpr (MOVED) {
+          uint32_t* xa = reinterpret_cast<uint32_t*>(smem + C::OFF_Q4);   // [tile][16 values][64 lanes]
+          if constexpr (XN >= 0) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) xa[(XN * 16 + v) * 64 + lane] = (uint32_t)c[MBW][XN][v];
+            wave_lds_sync();
+            epi_runs(std::integral_constant<int, 0>{}, std::integral_constant<int, MBW * 4>{});
+          } else {
+            epi_runs(std::integral_constant<int, 0>{}, std::integral_constant<int, MBW * 4>{});
+            wave_lds_sync();
+#pragma unroll
+            for (int v = 0; v < 16; ++v) c[MBW][MV][v] = (int)xa[(MV * 16 + v) * 64 + lane];
+            epi_runs(std::integral_constant<int, MBW * 4>{}, std::integral_constant<int, MBW * 4 + 4>{});
+          }
+        } else {
+          epi_runs(std::integral_constant<int, 0>{}, std::integral_constant<int, NAF * 4>{});
+        }
         if (has_next) store_consts((n_conv + 1) & 1, kn);
         __syncthreads();
       };
@@ -1858,9 +1885,10 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         }
     }
   };
-  if (wave == 0) trunk(std::integral_constant<int, 0>{});
-  else if (wave == 1) trunk(std::integral_constant<int, 1>{});
-  else trunk(std::integral_constant<int, -1>{});
+  if (wave == 0) trunk(std::integral_constant<int, 0>{}, std::integral_constant<int, -1>{});
+  else if (wave == 1) trunk(std::integral_constant<int, 1>{}, std::integral_constant<int, -1>{});
+  else if (wave == 2) trunk(std::integral_constant<int, -1>{}, std::integral_constant<int, MOVE ? 0 : -1>{});
+  else trunk(std::integral_constant<int, -1>{}, std::integral_constant<int, MOVE ? 1 : -1>{});
   __syncthreads();
   // ---- heads, shared by the four waves
   dep_heads4<MK>(p, smem, legal, policy, value, wdl, b, wave, lane);
