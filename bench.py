@@ -51,10 +51,10 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {  # (workload, tiling, batch): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
     ("net20x128_int8_b1024", 3, 1024): ("faf2c3970238b8113f568cabf1e9363b742d350fdec26bd0ffc19cbf57c667f6",
                                         33413.4, 18704.0),
-    ("deployed14x160_int8_b1024", 1, 1024): ("68cdf225840b036ee0f75ce815c89e8a98ac5cf960f2dc74dbe4a2f2f29029d3",
-                                             46253.9, 30140.0),
-    ("deployed14x160_int8_b1024", 2, 64): ("68cdf225840b036ee0f75ce815c89e8a98ac5cf960f2dc74dbe4a2f2f29029d3",
-                                           29236.0, 472.0),
+    ("deployed14x160_int8_b1024", 1, 1024): ("6d690c6d038c73c327bba8cf27932e64425ff1b2141ab7a2e8ca35aaa539713f",
+                                             46254.6, 30135.2),
+    ("deployed14x160_int8_b1024", 2, 64): ("6d690c6d038c73c327bba8cf27932e64425ff1b2141ab7a2e8ca35aaa539713f",
+                                           29403.9, 472.0),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
