@@ -729,16 +729,20 @@ constexpr int ring_depth(int want, int gpl) {
 template <int MK, int F>
 struct Sched {
   static constexpr int CPT = F / Mk<MK>::KS;
-  static constexpr bool BF = MK == MK_BF16;
-  // Multi-board tilings: int8 streams one step per group with a ring of 8
-  // (7 steps of prefetch), fp8 (32-byte fragments) a ring of 4, bf16 two-step
-  // groups with a ring of 2 (its fp32 residual stream needs the registers).
-  static constexpr int GL = BF ? 2 : 1, NL = BF ? 2 : (MK == MK_I8 ? 8 : 4), IL_L = 1;
-  static constexpr int GM = GL, NM = NL, IL_M = 1;
-  // small (one board per workgroup): one-step groups, ring of 8, except bf16 at
-  // F = 256, whose wider tile needs the registers for its residual stream
+  static constexpr bool BF = MK == MK_BF16, I8 = MK == MK_I8;
+  // Multi-board tilings: int8 streams one step per group with a ring of 12 in
+  // the large tiling (F <= 128) and 8 in the medium one (whose two workgroups per
+  // compute unit leave no registers for more), fp8 (32-byte fragments) a ring
+  // of 4, bf16 two-step groups with a ring of 2 (its fp32 residual stream needs
+  // the registers).
+  static constexpr int GL = BF ? 2 : 1, NL = BF ? 2 : (I8 ? (F <= 128 ? 12 : 8) : 4), IL_L = 1;
+  static constexpr int GM = GL, NM = BF ? 2 : (I8 ? 8 : 4), IL_M = 1;
+  // small (one board per workgroup): one-step groups; int8 a ring of 18 (a
+  // wave's K step is two MFMAs, so 17 steps of prefetch are needed to cover a
+  // load from the Infinity Cache), the others a ring of 8, bf16 at F = 256 two-step
+  // groups with a ring of 2 (the bf16 residual stream needs the registers)
   static constexpr bool W256 = BF && F == 256;
-  static constexpr int GS = W256 ? 2 : 1, NS = W256 ? 2 : 8, IL_S = 1;
+  static constexpr int GS = W256 ? 2 : 1, NS = W256 ? 2 : (I8 ? 18 : 8), IL_S = 1;
 };
 
 // Tilings (wave tile = MBW*32 channels x NBW half-boards):
