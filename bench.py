@@ -49,8 +49,10 @@ def kernel_source(shape):
 # for the kernel source it was taken on only: any other source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 TRAFFIC = {  # (workload, tiling, batch): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    ("net20x128_int8_b1024", 3, 1024): ("faf2c3970238b8113f568cabf1e9363b742d350fdec26bd0ffc19cbf57c667f6",
-                                        33413.4, 18704.0),
+    ("net20x128_int8_b1024", 3, 1024): ("b083df6631f8d72893c157c51fb6656f022bb036de3086877573cd955a8d5324",
+                                        33351.0, 18704.0),
+    ("net20x128_int8_b1024", 2, 64): ("b083df6631f8d72893c157c51fb6656f022bb036de3086877573cd955a8d5324",
+                                      24476.5, 1682.0),
     ("deployed14x160_int8_b1024", 1, 1024): ("6d690c6d038c73c327bba8cf27932e64425ff1b2141ab7a2e8ca35aaa539713f",
                                              46254.6, 30135.2),
     ("deployed14x160_int8_b1024", 2, 64): ("6d690c6d038c73c327bba8cf27932e64425ff1b2141ab7a2e8ca35aaa539713f",
