@@ -737,12 +737,13 @@ struct Sched {
   // the registers).
   static constexpr int GL = BF ? 2 : 1, NL = BF ? 2 : (I8 ? (F <= 128 ? 12 : 8) : 4), IL_L = 1;
   static constexpr int GM = GL, NM = BF ? 2 : (I8 ? 8 : 4), IL_M = 1;
-  // small (one board per workgroup): one-step groups; int8 a ring of 18 (a
-  // wave's K step is two MFMAs, so 17 steps of prefetch are needed to cover a
-  // load from the Infinity Cache), the others a ring of 8, bf16 at F = 256 two-step
-  // groups with a ring of 2 (the bf16 residual stream needs the registers)
+  // small (one board per workgroup): one-step groups; a wave's K step is two
+  // MFMAs, so covering a load from the Infinity Cache takes a deep ring: 18
+  // steps for int8, 12 for bf16 (measured best; 16 and 18 are slower or
+  // spill), 8 for fp8 (32-byte fragments); bf16 at F = 256 two-step groups with
+  // a ring of 2 (the bf16 residual stream needs the registers)
   static constexpr bool W256 = BF && F == 256;
-  static constexpr int GS = W256 ? 2 : 1, NS = W256 ? 2 : (I8 ? 18 : 8), IL_S = 1;
+  static constexpr int GS = W256 ? 2 : 1, NS = W256 ? 2 : (I8 ? 18 : (BF ? 12 : 8)), IL_S = 1;
 };
 
 // Tilings (wave tile = MBW*32 channels x NBW half-boards):
