@@ -53,10 +53,10 @@ TRAFFIC = {  # (workload, tiling, batch): (sha256 of the kernel source, FETCH_SI
                                         33355.5, 18704.0),
     ("net20x128_int8_b1024", 2, 64): ("4c515e7336b4aa547bc66fafbc48bc316a9268e850a3496fc96242f835cb37a5",
                                       24476.5, 1682.0),
-    ("deployed14x160_int8_b1024", 1, 1024): ("6d690c6d038c73c327bba8cf27932e64425ff1b2141ab7a2e8ca35aaa539713f",
-                                             46254.6, 30135.2),
-    ("deployed14x160_int8_b1024", 2, 64): ("6d690c6d038c73c327bba8cf27932e64425ff1b2141ab7a2e8ca35aaa539713f",
-                                           29403.9, 472.0),
+    ("deployed14x160_int8_b1024", 1, 1024): ("0dbc1335fc2eee0c035cb2fd72b845e67340d305a331eca66c22c0af0e2148ee",
+                                             46252.7, 30174.7),
+    ("deployed14x160_int8_b1024", 2, 64): ("0dbc1335fc2eee0c035cb2fd72b845e67340d305a331eca66c22c0af0e2148ee",
+                                           29524.5, 472.0),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.

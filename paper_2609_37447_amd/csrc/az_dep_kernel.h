@@ -1384,8 +1384,9 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
   // scalar and a block's a literal, so the loads cost no vector address
   // arithmetic.  K step i of the stream lives in ring slot i % NBUF, loaded
   // NBUF - 1 steps ahead: a wave's K step is two or three MFMAs, so the ring is
-  // deep enough to cover a load from L2 or the Infinity Cache.
-  constexpr int NBUF = 10;
+  // deep enough to cover a load from L2 or the Infinity Cache (int8 15 steps,
+  // bf16 10: measured best among the depths that tile two layers).
+  constexpr int NBUF = QUANT ? 15 : 10;
   static_assert((2 * C::S) % NBUF == 0, "every block's first conv starts at ring slot 0");
   const __amdgpu_buffer_rsrc_t twr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(p.tower_w), (short)0, (int)(2 * p.blocks * C::LAYER_BYTES), 0x00020000);
