@@ -125,7 +125,7 @@ typedef enum {
 typedef enum {
   AZ_OK = 0,
   AZ_ERR_INVALID_ARG = -1, /* NULL pointer, bad size or count, misaligned buffer */
-  AZ_ERR_UNSUPPORTED = -2, /* well-formed spec this build does not implement */
+  AZ_ERR_UNSUPPORTED = -2, /* well-formed spec the library does not implement */
   AZ_ERR_NOMEM = -3,       /* device allocation failed */
   AZ_ERR_DEVICE = -4       /* any other HIP runtime failure */
 } az_status;

@@ -95,7 +95,7 @@ hipError_t az_launch_f32(const AzDevNet& net, const float* planes, const uint8_t
 int az_mfma_boards_per_wg(int filters, int tiling);
 // Whether a tiling id (1 large, 2 small, 3 medium) exists for a filter count.
 bool az_mfma_tiling_valid(int filters, int tiling);
-// Whether an (dtype, filters) pair has MFMA kernels in this build.
+// Whether an (dtype, filters) pair has MFMA kernels in the library.
 bool az_mfma_supported(int dtype, int filters);
 // Records `detail` for az_last_error() and returns `status`.
 int az_fail(int status, const char* detail);
