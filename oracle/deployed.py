@@ -38,13 +38,14 @@ and are not scaled, pairs are ordered by (origin, destination) and promotions by
 
 Modes.
   forward(...)        float64 definition (parity reference for the bf16 path).
-  forward_quant(...)  the int8 network: residual convolutions on int8 codes as in
-                      az_oracle.forward_quant; the pooling step in floating point
-                      (Section 4.3: context operations stay in floating point
-                      inside the INT8 trunk): p in float32 from the exact integer
-                      accumulator, g and c in float64, c rounded once to float32,
-                      then added to the regular channels inside their
-                      requantisation; heads in floating point.
+  forward_quant(...)  the int8 network, the plain definition in float64:
+                      residual convolutions on int8 codes as in
+                      az_oracle.forward_quant; the pooling step in floating
+                      point (Section 4.3: context operations stay in floating
+                      point inside the INT8 trunk): the pooled channels'
+                      activations, their means and maxima and the projection c
+                      in float64, c added to the regular channels before their
+                      activation and requantisation; heads in floating point.
 """
 
 from __future__ import annotations
@@ -53,8 +54,7 @@ import math
 
 import numpy as np
 
-from .az_oracle import (N_SQUARES, _code, act, conv3x3, fma32, quant_params, quantize_weights,
-                        softmax_legal, to_bf16)
+from .az_oracle import N_SQUARES, act, conv3x3, quantize_weights, requant, softmax_legal, to_bf16
 
 N_PAIRS = 1792
 N_PROMOS = 88
@@ -247,40 +247,37 @@ def weight_scales(spec, blob, fmt="int8"):
     return np.concatenate(out).astype(np.float32)
 
 
-def pool_bias32(acc, m_in, b, cap, Wg):
-    """Pooled-context biases of one pooling block from the pooled channels'
-    exact accumulators: p = act(fma(acc, m_in, b)) in float32 (m_in = a_in * s_w
-    per channel), board means and maxima and their projection in float64,
-    rounded once to float32.  acc: [B, g, 8, 8]; returns [B, Fr] float32."""
-    f32 = np.float32
-    pz = fma32(np.asarray(acc, dtype=f32), np.asarray(m_in, dtype=f32)[None, :, None, None],
-               np.asarray(b, dtype=f32)[None, :, None, None])
-    p = np.maximum(pz, f32(0.0))
-    if cap and cap > 0:
-        p = np.minimum(p, f32(cap))
-    return (pool_features(p.astype(np.float64)) @ Wg.T).astype(f32)
+def pool_bias(acc, m_in, b, cap, Wg):
+    """Pooled-context biases of one pooling block of the int8 network: the pooled
+    channels' activations p = act(acc * m_in + b) (m_in = a_in * s_w per channel,
+    acc the exact sum of code products), their board means and maxima and the
+    projection c = Wg [mean, max], all float64 (Section 4.3: the context
+    operations stay in floating point inside the INT8 trunk).
+    acc: [B, g, 8, 8]; returns [B, Fr]."""
+    bc = lambda v: np.asarray(v, dtype=np.float64)[None, :, None, None]  # noqa: E731
+    p = act(np.asarray(acc, dtype=np.float64) * bc(m_in) + bc(b), cap)
+    return pool_features(p) @ np.asarray(Wg, dtype=np.float64).T
 
 
 def forward_quant(spec, blob, w_scales, act_scales, planes, legal, record=None):
-    """int8 deployed network.  Codes, scales and requantisation as in
-    az_oracle.forward_quant; in a pooling block the first convolution's regular
-    channels requantise as
-        z = fma(acc, Mq[f], Bq[f]);  z = fma(c[f], inv[n+1], z);  q = rne(clamp(z, 0, hi))
-    with c = pool_bias32 of the pooled channels (their codes are stored as
-    q = rne(clamp(fma(acc, Mq, Bq), 0, hi)) and feed nothing), and the second
-    convolution reads the Fr regular channels only."""
+    """int8 deployed network, the plain definition in float64.  Codes, scales and
+    requantisation as in az_oracle.forward_quant; in a pooling block the first
+    convolution's output y = acc * a[n] * s_w[f] + b1[f] splits into
+        pooled channels   p = act(y[Fr:])  (floating point, never quantised),
+                          c = pool_bias(...) = Wg [mean p, max p]
+        regular channels  q = sat(rne(act(y[:Fr] + c) / a[n+1]))
+    and the second convolution reads the Fr regular channels only."""
     fmt = "int8"
     F, nb = spec.filters, spec.blocks
     Fr = F - F // 4
     W = unpack(spec, blob)
-    sw = np.asarray(w_scales, dtype=np.float32).reshape(2 * nb, F)
-    a, inv, Mq, R, hi = quant_params(spec, w_scales, act_scales, fmt)
-    f32 = np.float32
+    sw = np.asarray(w_scales, dtype=np.float32).astype(np.float64).reshape(2 * nb, F)
+    a = np.asarray(act_scales, dtype=np.float32).astype(np.float64)
+    cap = spec.act_cap
+    bc = lambda v: v[None, :, None, None]  # noqa: E731
 
     x = to_bf16(np.asarray(planes, dtype=np.float64))
-    acc = conv3x3(x, W["stem.w"]).astype(f32)
-    b0 = (W["stem.b"].astype(f32) * inv[0]).astype(f32)
-    q = _code(fma32(acc, inv[0], b0[None, :, None, None]), hi[0], fmt)
+    q = requant(conv3x3(x, W["stem.w"], W["stem.b"]), a[0], cap, fmt)
     if record is not None:
         record.append(q)
     for j in range(nb):
@@ -288,26 +285,21 @@ def forward_quant(spec, blob, w_scales, act_scales, planes, legal, record=None):
         pool = is_pool_block(spec, j)
         # first convolution
         n = 2 * j
-        acc = conv3x3(q, quantize_weights(W[f"w1.{j}"], sw[n], fmt)).astype(f32)
-        b1 = W[f"b1.{j}"].astype(f32)
-        bq = (b1 * inv[n + 1]).astype(f32)
-        z = fma32(acc, Mq[n][None, :, None, None], bq[None, :, None, None])
+        acc = conv3x3(q, quantize_weights(W[f"w1.{j}"], sw[n], fmt))
+        y = acc * a[n] * bc(sw[n]) + bc(W[f"b1.{j}"])
         if pool:
-            m_in = (a[n] * sw[n]).astype(f32)
-            c = pool_bias32(acc[:, Fr:], m_in[Fr:], b1[Fr:], spec.act_cap, W[f"pool.{j}"])
-            z[:, :Fr] = fma32(c[:, :, None, None], inv[n + 1], z[:, :Fr])
-        q = _code(z, hi[n + 1], fmt)
-        if record is not None:
-            record.append(q[:, :Fr] if pool else q)
-        # second convolution (+ residual)
-        n = 2 * j + 1
-        qt = q[:, :Fr] if pool else q
-        acc = conv3x3(qt, quantize_weights(W[f"w2.{j}"], sw[n], fmt)).astype(f32)
-        bq = (W[f"b2.{j}"].astype(f32) * inv[n + 1]).astype(f32)
-        z = fma32(acc, Mq[n][None, :, None, None], bq[None, :, None, None])
-        z = fma32(q_in.astype(f32), R[n], z)
-        q = _code(z, hi[n + 1], fmt)
+            c = pool_bias(acc[:, Fr:], a[n] * sw[n][Fr:], W[f"b1.{j}"][Fr:], cap, W[f"pool.{j}"])
+            q = requant(y[:, :Fr] + c[:, :, None, None], a[n + 1], cap, fmt)
+        else:
+            q = requant(y, a[n + 1], cap, fmt)
         if record is not None:
             record.append(q)
-    h = q.astype(np.float64) * np.float64(a[2 * nb])
+        # second convolution (+ residual)
+        n = 2 * j + 1
+        acc = conv3x3(q, quantize_weights(W[f"w2.{j}"], sw[n], fmt))
+        y = acc * a[n] * bc(sw[n]) + bc(W[f"b2.{j}"]) + q_in * a[n - 1]
+        q = requant(y, a[n + 1], cap, fmt)
+        if record is not None:
+            record.append(q)
+    h = q * a[2 * nb]
     return heads(spec, W, h, legal)
