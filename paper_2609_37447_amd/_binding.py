@@ -27,7 +27,8 @@ EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_eval_batch_wdl
            "az_net_set_tiling",
            "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_compare_outputs",
            "az_pipeline_create", "az_pipeline_slot", "az_pipeline_submit", "az_pipeline_query",
-           "az_pipeline_wait", "az_pipeline_free", "az_status_string", "az_last_error")
+           "az_pipeline_wait", "az_pipeline_free", "az_debug_fail_allocation", "az_debug_live_allocations",
+           "az_status_string", "az_last_error")
 
 
 class az_layer_spec(ctypes.Structure):
@@ -90,6 +91,8 @@ def lib():
         L.az_pipeline_query.argtypes, L.az_pipeline_query.restype = [P, I32], ctypes.c_int
         L.az_pipeline_wait.argtypes, L.az_pipeline_wait.restype = [P, I32], ctypes.c_int
         L.az_pipeline_free.argtypes, L.az_pipeline_free.restype = [P], None
+        L.az_debug_fail_allocation.argtypes, L.az_debug_fail_allocation.restype = [I32], None
+        L.az_debug_live_allocations.argtypes, L.az_debug_live_allocations.restype = [], ctypes.c_int64
         L.az_status_string.argtypes, L.az_status_string.restype = [ctypes.c_int], ctypes.c_char_p
         L.az_last_error.argtypes, L.az_last_error.restype = [], ctypes.c_char_p
         _lib = L
@@ -187,6 +190,14 @@ def az_net_free(net) -> None:
     lib().az_net_free(net)
 
 
+def az_debug_fail_allocation(n: int) -> None:
+    lib().az_debug_fail_allocation(int(n))
+
+
+def az_debug_live_allocations() -> int:
+    return int(lib().az_debug_live_allocations())
+
+
 def az_status_string(status: int) -> str:
     return lib().az_status_string(int(status)).decode()
 
@@ -269,10 +280,14 @@ AZ_PIPE_GRAPHS = 1
 AZ_PIPE_COMPACT_POLICY = 2
 
 
-def az_pipeline_create(net, max_batch: int, slots: int, flags: int = 0, max_legal: int = 0):
+def az_pipeline_create(net, max_batch: int, slots: int, flags: int = 0, max_legal: int = 0,
+                       raise_on_error: bool = True):
+    """Returns the pipeline handle, or (status) when raise_on_error is False and it fails."""
     out = ctypes.c_void_p()
-    _check(lib().az_pipeline_create(net, max_batch, slots, flags, max_legal, ctypes.byref(out)),
-           "az_pipeline_create")
+    st = lib().az_pipeline_create(net, max_batch, slots, flags, max_legal, ctypes.byref(out))
+    if st != AZ_OK and not raise_on_error:
+        return st
+    _check(st, "az_pipeline_create")
     return out
 
 

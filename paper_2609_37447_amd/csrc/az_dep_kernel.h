@@ -25,11 +25,13 @@
 // bank slot their virtual square would use.
 //
 // Global pooling (every pool_every-th block).  After the first convolution's
-// K loop, the pooled channels (the last F/4) are activated from the
-// accumulators and transposed through LDS; one lane per pooled channel reduces
-// its board sum (fp64) and maximum, and the projection c = Wg [mean, max] runs
-// in fp64, one or two outputs per lane; c (rounded to fp32) is then added to
-// the regular channels in the same epilogue that writes them.
+// K loop, the pooled channels (the last F/4) are transposed through LDS (int8:
+// the exact accumulators; bf16: their activations); one lane per pooled
+// channel activates (int8, in float64) and reduces its row to a board sum
+// (fp64) and maximum, and the projection c = Wg [mean, max] runs in fp64, one
+// or two outputs per lane.  c is added to the regular channels' bias in the
+// layer's constant slot (int8: in code units, in float64), so the epilogue
+// that writes them takes it with the bias.
 //
 // bf16 networks carry the residual stream h as hi + lo: hi = bf16(h) is the
 // convolution operand in LDS, lo = bf16(h - hi) stays in the registers of the
@@ -99,6 +101,53 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Board maximum (x) and sum (y) of pooled row pc of a pooling layer (first conv
+// n_conv), read from LDS rows [pooled channel][square] with 16-byte chunks
+// XOR-swizzled by the row.  int8 rows hold the exact accumulators, activated
+// here in float64: act(acc * a[n] * s_w[f] + b1[f]); bf16 rows hold the
+// activations.
+template <bool QUANT>
+__device__ __forceinline__ double2 pool_row(const AzDevNet& p, const float* pt, int pc, int n_conv) {
+  double sum = 0.0, mx = 0.0;  // activations are >= 0
+  if constexpr (QUANT) {
+    const size_t o = (size_t)n_conv * DF + DFR + pc;
+    const double pm = p.pool_m[o], pb = p.pool_b[o], cap = p.act_cap;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int4 v = *reinterpret_cast<const int4*>(pt + pc * 64 + ((j ^ (pc & 15)) << 2));
+      const int vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const double a = clamp_d(__builtin_fma((double)vv[r], pm, pb), cap);
+        sum += a;
+        mx = __builtin_fmax(mx, a);
+      }
+    }
+  } else {
+    float mxf = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const float4 v = *reinterpret_cast<const float4*>(pt + pc * 64 + ((j ^ (pc & 15)) << 2));
+      sum += (double)v.x;
+      sum += (double)v.y;
+      sum += (double)v.z;
+      sum += (double)v.w;
+      mxf = fmaxf(mxf, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+    }
+    mx = mxf;
+  }
+  return make_double2(mx, sum);
+}
+
+// Folds the projected context c[o] of a pooling layer into regular channel o's
+// bias in the layer's constant slot: int8 slots hold qbias = b / a[n+1] in
+// float64, so c enters in code units (c / a[n+1]); bf16 slots hold b in fp32.
+template <bool QUANT>
+__device__ __forceinline__ void add_context(const AzDevNet& p, float* kslot, int o, double c, int n_conv) {
+  if constexpr (QUANT) reinterpret_cast<double*>(kslot)[o] += c * p.pool_cinv[n_conv];
+  else kslot[o] += (float)c;
+}
+
 // bf16 hi and lo parts of eight fp32 values: x = hi + lo within 2^-16 |x|.
 __device__ __forceinline__ void split8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
   uint32_t h[4], l[4];
@@ -131,11 +180,12 @@ struct DepCfg {
   static constexpr int BUF = 64 * RB;
   static constexpr int OFF_H = 0, OFF_T = BUF, OFF_Z = 2 * BUF;
   static constexpr int ZB = (RB + 256 + 255) / 256 * 256;
-  static constexpr int KSLOT = 4 * DF * 4;            // [bias F | qmul F | pool m F | pool b F] floats
+  // per-layer epilogue constants: [bias F] floats, or for int8 [qbias F | qmul F]
+  // doubles (the float64 requantisation)
+  static constexpr int KSLOT = QUANT ? 16 * DF : 4 * DF;
   static constexpr int OFF_K = OFF_Z + ZB;
   static constexpr int OFF_PG = OFF_K + 2 * KSLOT;    // pooled statistics, 2g doubles
-  static constexpr int OFF_C = OFF_PG + 2 * DG * 8;   // projected biases, F floats
-  static constexpr int TOWER_END = OFF_C + DF * 4;
+  static constexpr int TOWER_END = OFF_PG + 2 * DG * 8;
   static constexpr int OFF_X = BUF;                   // heads' bf16 input: the lo part (bf16 networks)
   static constexpr int X_END = QUANT ? 0 : OFF_X + 64 * RBX;
   static constexpr int OFF_S = 0;                     // query-key logits [64][64] f32
@@ -828,7 +878,6 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
   for (int i = lane; i < C::ZB / 16; i += 64)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
-  for (int i = lane; i < DF; i += 64) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
   {
     // item k = planes 8k..8k+7: lane = square, eight coalesced loads, one
     // 16-byte store
@@ -866,21 +915,19 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     for (int m = 0; m < DNMB; ++m)
       dst[m] = __builtin_bit_cast(frag_t, __builtin_amdgcn_raw_buffer_load_b128(twr, tvoff, soff + m * 64 * T::FB, 0));
   };
-  // per-layer epilogue constants [bias F | qmul F | pool m F | pool b F] of conv
-  // index k (0 = stem; the pooling constants of conv k - 1): lane-held float4s
-  // (10 floats per lane), loaded at the start of a layer and parked in LDS
-  // before its barrier
-  constexpr int KV = 4 * DF / 4;                     // float4s per slot
+  // per-layer epilogue constants of conv index k (0 = stem): [bias F] floats, or
+  // [qbias F | qmul F] doubles, as lane-held 16-byte chunks loaded at the start
+  // of a layer and parked in LDS before its barrier
+  constexpr int KV = C::KSLOT / 16;                  // 16-byte chunks per slot
   constexpr int KPL = (KV + 63) / 64;                // per lane
   auto load_consts = [&](int k, float4(&dst)[KPL]) {
 #pragma unroll
     for (int t = 0; t < KPL; ++t) {
-      const int i = lane + 64 * t, arr = i / (DF / 4), off = 4 * (i % (DF / 4));
-      const float* src = arr == 0 ? p.bias + (size_t)k * DF
-                       : arr == 1 ? (QUANT ? p.qmul + (size_t)k * DF : p.bias)
-                       : arr == 2 ? p.pool_m + (size_t)(k - 1) * DF
-                                  : p.pool_b + (size_t)(k - 1) * DF;
-      dst[t] = i < KV ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int i = lane + 64 * t;
+      const void* src;
+      if constexpr (QUANT) src = i < DF / 2 ? p.qbias + (size_t)k * DF + 2 * i : p.qmul + (size_t)k * DF + 2 * (i - DF / 2);
+      else src = p.bias + (size_t)k * DF + 4 * i;
+      dst[t] = i < KV ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   auto store_consts = [&](int slot, const float4(&v)[KPL]) {
@@ -960,8 +1007,14 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       for (int q = 0; q < 4; ++q) {
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
         const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
-        float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
-        if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
+        double mq[4] = {}, bq[4] = {};
+        if constexpr (QUANT) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            mq[r] = p.qmul[ch0 + r];
+            bq[r] = p.qbias[ch0 + r];
+          }
+        }
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
           const int j = n * 32 + l32;
@@ -974,13 +1027,12 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             *reinterpret_cast<uint2*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi) =
                 make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
           } else {
-            const float hi = p.qhi[0];
-            const float z0 = med3(__builtin_fmaf(v[4 * q + 0], mm.x, bb.x), 0.0f, hi);
-            const float z1 = med3(__builtin_fmaf(v[4 * q + 1], mm.y, bb.y), 0.0f, hi);
-            const float z2 = med3(__builtin_fmaf(v[4 * q + 2], mm.z, bb.z), 0.0f, hi);
-            const float z3 = med3(__builtin_fmaf(v[4 * q + 3], mm.w, bb.w), 0.0f, hi);
+            // fp32 sum of the bf16 matrix instruction; rescale and rounding in float64
             *reinterpret_cast<uint32_t*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15)) =
-                pack_codes<MK>(z0, z1, z2, z3);
+                pack_codes_d<MK>(__builtin_fma((double)v[4 * q + 0], mq[0], bq[0]),
+                                 __builtin_fma((double)v[4 * q + 1], mq[1], bq[1]),
+                                 __builtin_fma((double)v[4 * q + 2], mq[2], bq[2]),
+                                 __builtin_fma((double)v[4 * q + 3], mq[3], bq[3]), p.qhi[0]);
           }
         }
       }
@@ -1007,7 +1059,7 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       const bool has_next = n_conv + 1 < nconv;
       const int in_off = SECOND ? OFF_T : OFF_H;
       const int out_off = SECOND ? OFF_H : OFF_T;
-      const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
+      float* kslot = reinterpret_cast<float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
       // the next layer's epilogue constants, in flight during this layer
       float4 kn[KPL];
       if (has_next) load_consts(n_conv + 2, kn);
@@ -1101,31 +1153,31 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         tap_body(std::integral_constant<int, (LB + t * CPT) % NBUF>{}, std::false_type{}, t);
       });
 
-      // global pooling: pooled channels' board mean and maximum, projection to
-      // the regular channels' biases (LDS OFF_C)
-      float cinv = 1.0f;
+      // global pooling: pooled channels' board mean and maximum, projected to a
+      // context term that is folded into the regular channels' bias (in place in
+      // this layer's constant slot)
       if constexpr (POOL) {
-        cinv = p.pool_cinv[n_conv];
-        // (1) pooled activations to LDS as [pooled channel][square] f32 in the T
+        // (1) the pooled channels to LDS as [pooled channel][square] in the T
         //     buffer (written by this layer's epilogue only afterwards); rows of
-        //     256 bytes with 16-byte chunks XOR-swizzled by the row
+        //     256 bytes with 16-byte chunks XOR-swizzled by the row.  int8: the
+        //     exact accumulators, activated in float64 in (2); bf16: act(acc + b1)
         float* pt = reinterpret_cast<float*>(smem + OFF_T);
         static_assert(DG * 64 * 4 <= C::BUF, "pooled activations fit in the T buffer");
         static_for<0, DNMB * 4>([&](auto k_c) {
           constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4;
           if constexpr (32 * m + 8 * q >= DFR) {
             const int ch0 = 32 * m + 8 * q + 4 * lhi;
-            const float4 mm = *reinterpret_cast<const float4*>(kslot + 2 * DF + ch0);
-            const float4 bb = *reinterpret_cast<const float4*>(kslot + 3 * DF + ch0);
-            const float mv[4] = {mm.x, mm.y, mm.z, mm.w}, bv[4] = {bb.x, bb.y, bb.z, bb.w};
+            float4 bb = make_float4(0.f, 0.f, 0.f, 0.f);
+            if constexpr (!QUANT) bb = *reinterpret_cast<const float4*>(kslot + ch0);
+            const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int pc = ch0 + r - DFR;
 #pragma unroll
               for (int n = 0; n < NBW; ++n) {
-                const int sq = 32 * n + l32;
-                pt[pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3)] =
-                    med3(__builtin_fmaf((float)c[m][n][4 * q + r], mv[r], bv[r]), 0.0f, cap);
+                const int sq = 32 * n + l32, idx = pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3);
+                if constexpr (QUANT) reinterpret_cast<int*>(pt)[idx] = (int)c[m][n][4 * q + r];
+                else pt[idx] = med3(c[m][n][4 * q + r] + bv[r], 0.0f, cap);
               }
             }
           }
@@ -1134,19 +1186,9 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         // (2) lane pc < g: board sum (fp64) and maximum of its row; g = [mean, max]
         double* pg = reinterpret_cast<double*>(smem + C::OFF_PG);
         if (lane < DG) {
-          double sum = 0.0;
-          float mx = 0.0f;  // activations are >= 0
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const float4 v = *reinterpret_cast<const float4*>(pt + lane * 64 + ((j ^ (lane & 15)) << 2));
-            sum += (double)v.x;
-            sum += (double)v.y;
-            sum += (double)v.z;
-            sum += (double)v.w;
-            mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
-          }
-          pg[lane] = sum * (1.0 / 64.0);
-          pg[DG + lane] = (double)mx;
+          const double2 mx_sum = pool_row<QUANT>(p, pt, lane, n_conv);
+          pg[lane] = mx_sum.y * (1.0 / 64.0);
+          pg[DG + lane] = mx_sum.x;
         }
         wave_lds_sync();
         // (3) c[o] = sum_i Wg[o][i] g[i] in fp64 (fp32 weights are exact): lane L
@@ -1182,23 +1224,26 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             c1 = __builtin_fma((double)w1.w, gi[3], c1);
           }
         }
-        float* cb = reinterpret_cast<float*>(smem + C::OFF_C);
-        cb[lane] = (float)c0;
-        if (lane + 64 < DFR) cb[lane + 64] = (float)c1;
+        // regular channel o's bias takes c[o] (int8: in code units, c[o] / a[n+1])
+        add_context<QUANT>(p, kslot, lane, c0, n_conv);
+        if (lane + 64 < DFR) add_context<QUANT>(p, kslot, lane + 64, c1, n_conv);
         wave_lds_sync();
       }
 
       // epilogue: per run of 4 channels; LDS reads of constants (and residual
       // codes) issued two runs ahead
-      float hi = 0.0f, rq = 0.0f;
+      double hi = 0.0, rq = 0.0;
       if constexpr (QUANT) {
         hi = p.qhi[n_conv + 1];
-        rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
+        rq = SECOND ? p.qres[n_conv + 1] : 0.0;
       }
       constexpr int NRUN = DNMB * 4, EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
       constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
       constexpr bool RHI = !QUANT && SECOND;    // residual hi parts, read in place
-      float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
+      // int8 constants: qbias and qmul of the run's four channels, float64
+      struct KQ { double b[4], m[4]; };
+      float4 kb[QUANT ? 1 : EP_RING];
+      KQ kq[QUANT ? EP_RING : 1];
       uint32_t rcode[RCODE ? EP_RING : 1][NBW];
       uint2 rhi[RHI ? EP_RING : 1][NBW];
       auto ep_addr = [&](int m, int q, int n) {
@@ -1211,9 +1256,20 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       auto ep_load = [&](auto k_c) {
         constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
         const int ch0 = m * 32 + 8 * q + 4 * lhi;
-        kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
-        if constexpr (QUANT) km[slot] = *reinterpret_cast<const float4*>(kslot + DF + ch0);
-        if constexpr (POOL) kc[slot] = *reinterpret_cast<const float4*>(smem + C::OFF_C + ch0 * 4);
+        if constexpr (QUANT) {
+          const double* kd = reinterpret_cast<const double*>(kslot);
+#pragma unroll
+          for (int r = 0; r < 4; r += 2) {
+            const double2 b2 = *reinterpret_cast<const double2*>(kd + ch0 + r);
+            const double2 m2 = *reinterpret_cast<const double2*>(kd + DF + ch0 + r);
+            kq[slot].b[r] = b2.x;
+            kq[slot].b[r + 1] = b2.y;
+            kq[slot].m[r] = m2.x;
+            kq[slot].m[r + 1] = m2.y;
+          }
+        } else {
+          kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
+        }
         if constexpr (RCODE) {
 #pragma unroll
           for (int n = 0; n < NBW; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
@@ -1227,21 +1283,14 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       static_for<0, NRUN>([&](auto k_c) {
         constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
         if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
-        const float4 bb = kb[slot];
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
           const int addr = ep_addr(m, q, n);
           const acc_t& v = c[m][n];
           if constexpr (!QUANT) {
+            const float4 bb = kb[slot];
             float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
             float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
-            if constexpr (POOL) {
-              const float4 cc = kc[slot];
-              y0 += cc.x;
-              y1 += cc.y;
-              y2 += cc.z;
-              y3 += cc.w;
-            }
             if constexpr (SECOND) {
               // block input h = hi + lo (exact in fp32)
               const uint2 hv = rhi[slot][n];
@@ -1260,27 +1309,19 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             }
             *reinterpret_cast<uint2*>(smem + addr) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
           } else {
-            const float4 mm = km[slot];
-            float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
-            float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
-            float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
-            float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
-            if constexpr (POOL) {
-              const float4 cc = kc[slot];
-              z0 = __builtin_fmaf(cc.x, cinv, z0);
-              z1 = __builtin_fmaf(cc.y, cinv, z1);
-              z2 = __builtin_fmaf(cc.z, cinv, z2);
-              z3 = __builtin_fmaf(cc.w, cinv, z3);
-            }
+            // float64 requantisation: z = acc * qmul + qbias (+ residual code * qres)
+            const KQ& kk = kq[slot];
+            double z[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) z[r] = __builtin_fma((double)v[4 * q + r], kk.m[r], kk.b[r]);
             if constexpr (SECOND) {
-              const uint32_t r = rcode[slot][n];
-              z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
-              z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
-              z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
-              z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
+              const uint32_t rc = rcode[slot][n];
+              z[0] = __builtin_fma((double)code_value<MK, 0>(rc), rq, z[0]);
+              z[1] = __builtin_fma((double)code_value<MK, 1>(rc), rq, z[1]);
+              z[2] = __builtin_fma((double)code_value<MK, 2>(rc), rq, z[2]);
+              z[3] = __builtin_fma((double)code_value<MK, 3>(rc), rq, z[3]);
             }
-            *reinterpret_cast<uint32_t*>(smem + addr) =
-                pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi), med3(z3, 0.0f, hi));
+            *reinterpret_cast<uint32_t*>(smem + addr) = pack_codes_d<MK>(z[0], z[1], z[2], z[3], hi);
           }
         }
       });
@@ -1354,7 +1395,6 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
   // ---- ingest: zero region, planes -> bf16 [square][64 channels] at OFF_T
   for (int i = tid; i < C::ZB / 16; i += NT)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
-  for (int i = tid; i < DF; i += NT) reinterpret_cast<float*>(smem + C::OFF_C)[i] = 0.0f;
   {
     // item k = planes 8k..8k+7 (items wave, wave + NWB, ...): lane = square,
     // eight coalesced loads, one 16-byte store
@@ -1392,20 +1432,19 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
       const_cast<void*>(p.tower_w), (short)0, (int)(2 * p.blocks * C::LAYER_BYTES), 0x00020000);
   const int tvoff = (mb0 * 64 + lane) * T::FB;
   const int tvoffx = ((DNMB - 1) * 64 + lane) * T::FB;
-  // per-layer epilogue constants [bias F | qmul F | pool m F | pool b F] of conv
-  // index k (0 = stem; the pooling constants of conv k - 1): thread-held float4s,
-  // loaded at the start of a layer and parked in LDS before its barrier
-  constexpr int KV = 4 * DF / 4;                     // float4s per slot
+  // per-layer epilogue constants of conv index k (0 = stem): [bias F] floats, or
+  // [qbias F | qmul F] doubles, as thread-held 16-byte chunks loaded at the start
+  // of a layer and parked in LDS before its barrier
+  constexpr int KV = C::KSLOT / 16;                  // 16-byte chunks per slot
   constexpr int KPL = (KV + NT - 1) / NT;            // per thread
   auto load_consts = [&](int k, float4(&dst)[KPL]) {
 #pragma unroll
     for (int t = 0; t < KPL; ++t) {
-      const int i = tid + NT * t, arr = i / (DF / 4), off = 4 * (i % (DF / 4));
-      const float* src = arr == 0 ? p.bias + (size_t)k * DF
-                       : arr == 1 ? (QUANT ? p.qmul + (size_t)k * DF : p.bias)
-                       : arr == 2 ? p.pool_m + (size_t)(k - 1) * DF
-                                  : p.pool_b + (size_t)(k - 1) * DF;
-      dst[t] = i < KV ? *reinterpret_cast<const float4*>(src + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int i = tid + NT * t;
+      const void* src;
+      if constexpr (QUANT) src = i < DF / 2 ? p.qbias + (size_t)k * DF + 2 * i : p.qmul + (size_t)k * DF + 2 * (i - DF / 2);
+      else src = p.bias + (size_t)k * DF + 4 * i;
+      dst[t] = i < KV ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   auto store_consts = [&](int slot, const float4(&v)[KPL]) {
@@ -1516,8 +1555,14 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         for (int q = 0; q < 4; ++q) {
           const int ch0 = blk_of(m) * 32 + 8 * q + 4 * lhi;
           const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
-          float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
-          if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
+          double mq[4] = {}, bq[4] = {};
+          if constexpr (QUANT) {
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              mq[r] = p.qmul[ch0 + r];
+              bq[r] = p.qbias[ch0 + r];
+            }
+          }
 #pragma unroll
           for (int n = n_lo(m); n < n_hi(m); ++n) {
             const int j = n * 32 + l32;
@@ -1530,13 +1575,12 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
               *reinterpret_cast<uint2*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 3, R::sw(j)) << 4) + 8 * lhi) =
                   make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
             } else {
-              const float hi = p.qhi[0];
-              const float z0 = med3(__builtin_fmaf(v[4 * q + 0], mm.x, bb.x), 0.0f, hi);
-              const float z1 = med3(__builtin_fmaf(v[4 * q + 1], mm.y, bb.y), 0.0f, hi);
-              const float z2 = med3(__builtin_fmaf(v[4 * q + 2], mm.z, bb.z), 0.0f, hi);
-              const float z3 = med3(__builtin_fmaf(v[4 * q + 3], mm.w, bb.w), 0.0f, hi);
+              // fp32 sum of the bf16 matrix instruction; rescale and rounding in float64
               *reinterpret_cast<uint32_t*>(smem + OFF_H + j * RB + (R::pos(ch0 >> 4, R::sw(j)) << 4) + (ch0 & 15)) =
-                  pack_codes<MK>(z0, z1, z2, z3);
+                  pack_codes_d<MK>(__builtin_fma((double)v[4 * q + 0], mq[0], bq[0]),
+                                   __builtin_fma((double)v[4 * q + 1], mq[1], bq[1]),
+                                   __builtin_fma((double)v[4 * q + 2], mq[2], bq[2]),
+                                   __builtin_fma((double)v[4 * q + 3], mq[3], bq[3]), p.qhi[0]);
             }
           }
         }
@@ -1563,7 +1607,7 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         const bool has_next = n_conv + 1 < nconv;
         const int in_off = SECOND ? OFF_T : OFF_H;
         const int out_off = SECOND ? OFF_H : OFF_T;
-        const float* kslot = reinterpret_cast<const float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
+        float* kslot = reinterpret_cast<float*>(smem + C::OFF_K + (n_conv & 1) * C::KSLOT);
         // the next layer's epilogue constants, in flight during this layer
         float4 kn[KPL];
         if (has_next) load_consts(n_conv + 2, kn);
@@ -1667,31 +1711,31 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
           tap_body(std::integral_constant<int, (LB + t * CPT) % NBUF>{}, std::false_type{}, t);
         });
 
-        // global pooling: pooled channels' board mean and maximum, projection to
-        // the regular channels' biases (LDS OFF_C)
-        float cinv = 1.0f;
+        // global pooling: pooled channels' board mean and maximum, projected to a
+        // context term that is folded into the regular channels' bias (in place in
+        // this layer's constant slot)
         if constexpr (POOL) {
-          cinv = p.pool_cinv[n_conv];
-          // (1) pooled activations to LDS as [pooled channel][square] f32 in the T
+          // (1) the pooled channels to LDS as [pooled channel][square] in the T
           //     buffer (written by this layer's epilogue only afterwards); rows of
-          //     256 bytes with 16-byte chunks XOR-swizzled by the row
+          //     256 bytes with 16-byte chunks XOR-swizzled by the row.  int8: the
+          //     exact accumulators, activated in float64 in (2); bf16: act(acc + b1)
           float* pt = reinterpret_cast<float*>(smem + OFF_T);
           static_assert(DG * 64 * 4 <= C::BUF, "pooled activations fit in the T buffer");
           static_for<0, NAF * 4>([&](auto k_c) {
             constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4;
             if (32 * blk_of(m) + 8 * q >= DFR) {
               const int ch0 = 32 * blk_of(m) + 8 * q + 4 * lhi;
-              const float4 mm = *reinterpret_cast<const float4*>(kslot + 2 * DF + ch0);
-              const float4 bb = *reinterpret_cast<const float4*>(kslot + 3 * DF + ch0);
-              const float mv[4] = {mm.x, mm.y, mm.z, mm.w}, bv[4] = {bb.x, bb.y, bb.z, bb.w};
+              float4 bb = make_float4(0.f, 0.f, 0.f, 0.f);
+              if constexpr (!QUANT) bb = *reinterpret_cast<const float4*>(kslot + ch0);
+              const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const int pc = ch0 + r - DFR;
 #pragma unroll
                 for (int n = n_lo(m); n < n_hi(m); ++n) {
-                  const int sq = 32 * n + l32;
-                  pt[pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3)] =
-                      med3(__builtin_fmaf((float)c[m][n][4 * q + r], mv[r], bv[r]), 0.0f, cap);
+                  const int sq = 32 * n + l32, idx = pc * 64 + (((sq >> 2) ^ (pc & 15)) << 2) + (sq & 3);
+                  if constexpr (QUANT) reinterpret_cast<int*>(pt)[idx] = (int)c[m][n][4 * q + r];
+                  else pt[idx] = med3(c[m][n][4 * q + r] + bv[r], 0.0f, cap);
                 }
               }
             }
@@ -1703,19 +1747,9 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
           static_assert(DG % 4 == 0, "pooled rows per wave");
           if (lane < DG / 4) {
             const int pc = (DG / 4) * wave + lane;
-            double sum = 0.0;
-            float mx = 0.0f;  // activations are >= 0
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-              const float4 v = *reinterpret_cast<const float4*>(pt + pc * 64 + ((j ^ (pc & 15)) << 2));
-              sum += (double)v.x;
-              sum += (double)v.y;
-              sum += (double)v.z;
-              sum += (double)v.w;
-              mx = fmaxf(mx, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
-            }
-            pg[pc] = sum * (1.0 / 64.0);
-            pg[DG + pc] = (double)mx;
+            const double2 mx_sum = pool_row<QUANT>(p, pt, pc, n_conv);
+            pg[pc] = mx_sum.y * (1.0 / 64.0);
+            pg[DG + pc] = mx_sum.x;
           }
           wave_lds_sync();
           // (3) c[o] = sum_i Wg[o][i] g[i] in fp64 (fp32 weights are exact): waves 0
@@ -1732,22 +1766,26 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
               co = __builtin_fma((double)w.z, gi[2], co);
               co = __builtin_fma((double)w.w, gi[3], co);
             }
-            if (o < DFR) reinterpret_cast<float*>(smem + C::OFF_C)[o] = (float)co;
+            // regular channel o's bias takes c[o] (int8: in code units, c[o] / a[n+1])
+            if (o < DFR) add_context<QUANT>(p, kslot, o, co, n_conv);
           }
           wave_lds_sync();
         }
 
         // epilogue: per run of 4 channels; LDS reads of constants (and residual
         // codes) issued two runs ahead
-        float hi = 0.0f, rq = 0.0f;
+        double hi = 0.0, rq = 0.0;
         if constexpr (QUANT) {
           hi = p.qhi[n_conv + 1];
-          rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
+          rq = SECOND ? p.qres[n_conv + 1] : 0.0;
         }
         constexpr int EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
         constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
         constexpr bool RHI = !QUANT && SECOND;    // residual hi parts, read in place
-        float4 kb[EP_RING], km[QUANT ? EP_RING : 1], kc[POOL ? EP_RING : 1];
+        // int8 constants: qbias and qmul of the run's four channels, float64
+        struct KQ { double b[4], m[4]; };
+        float4 kb[QUANT ? 1 : EP_RING];
+        KQ kq[QUANT ? EP_RING : 1];
         uint32_t rcode[RCODE ? EP_RING : 1][NBW];
         uint2 rhi[RHI ? EP_RING : 1][NBW];
         auto ep_addr = [&](int m, int q, int n) {
@@ -1760,9 +1798,20 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         auto ep_load = [&](auto k_c) {
           constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
           const int ch0 = blk_of(m) * 32 + 8 * q + 4 * lhi;
-          kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
-          if constexpr (QUANT) km[slot] = *reinterpret_cast<const float4*>(kslot + DF + ch0);
-          if constexpr (POOL) kc[slot] = *reinterpret_cast<const float4*>(smem + C::OFF_C + ch0 * 4);
+          if constexpr (QUANT) {
+            const double* kd = reinterpret_cast<const double*>(kslot);
+  #pragma unroll
+            for (int r = 0; r < 4; r += 2) {
+              const double2 b2 = *reinterpret_cast<const double2*>(kd + ch0 + r);
+              const double2 m2 = *reinterpret_cast<const double2*>(kd + DF + ch0 + r);
+              kq[slot].b[r] = b2.x;
+              kq[slot].b[r + 1] = b2.y;
+              kq[slot].m[r] = m2.x;
+              kq[slot].m[r + 1] = m2.y;
+            }
+          } else {
+            kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
+          }
           if constexpr (RCODE) {
 #pragma unroll
             for (int n = n_lo(m); n < n_hi(m); ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
@@ -1779,21 +1828,14 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         static_for<K0, K1>([&](auto k_c) {
           constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
           if constexpr (k + EP_AHEAD < K1) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
-          const float4 bb = kb[slot];
 #pragma unroll
           for (int n = n_lo(m); n < n_hi(m); ++n) {
             const int addr = ep_addr(m, q, n);
             const acc_t& v = c[m][n];
             if constexpr (!QUANT) {
+              const float4 bb = kb[slot];
               float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
               float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
-              if constexpr (POOL) {
-                const float4 cc = kc[slot];
-                y0 += cc.x;
-                y1 += cc.y;
-                y2 += cc.z;
-                y3 += cc.w;
-              }
               if constexpr (SECOND) {
                 // block input h = hi + lo (exact in fp32)
                 const uint2 hv = rhi[slot][n];
@@ -1812,27 +1854,19 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
               }
               *reinterpret_cast<uint2*>(smem + addr) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
             } else {
-              const float4 mm = km[slot];
-              float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
-              float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
-              float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
-              float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
-              if constexpr (POOL) {
-                const float4 cc = kc[slot];
-                z0 = __builtin_fmaf(cc.x, cinv, z0);
-                z1 = __builtin_fmaf(cc.y, cinv, z1);
-                z2 = __builtin_fmaf(cc.z, cinv, z2);
-                z3 = __builtin_fmaf(cc.w, cinv, z3);
-              }
+              // float64 requantisation: z = acc * qmul + qbias (+ residual code * qres)
+              const KQ& kk = kq[slot];
+              double z[4];
+  #pragma unroll
+              for (int r = 0; r < 4; ++r) z[r] = __builtin_fma((double)v[4 * q + r], kk.m[r], kk.b[r]);
               if constexpr (SECOND) {
-                const uint32_t r = rcode[slot][n];
-                z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
-                z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
-                z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
-                z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
+                const uint32_t rc = rcode[slot][n];
+                z[0] = __builtin_fma((double)code_value<MK, 0>(rc), rq, z[0]);
+                z[1] = __builtin_fma((double)code_value<MK, 1>(rc), rq, z[1]);
+                z[2] = __builtin_fma((double)code_value<MK, 2>(rc), rq, z[2]);
+                z[3] = __builtin_fma((double)code_value<MK, 3>(rc), rq, z[3]);
               }
-              *reinterpret_cast<uint32_t*>(smem + addr) =
-                  pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi), med3(z3, 0.0f, hi));
+              *reinterpret_cast<uint32_t*>(smem + addr) = pack_codes_d<MK>(z[0], z[1], z[2], z[3], hi);
             }
           }
         });

@@ -25,18 +25,21 @@ struct AzDevNet {
   const void* tower_w;
   const void* head_w;
   // Per-channel epilogue constants, [(1 + 2*blocks) * F]: the stem, then residual
-  // conv n = 0..2*blocks-1.  Float nets: bias = b.  Quantised nets: the
-  // requantising multiply-add z = fma(acc, qmul, bias) with
-  //   stem:   qmul = 1/a[0],                       bias = b * (1/a[0])
-  //   conv n: qmul = (a[n] * s_w[n][f]) * (1/a[n+1]), bias = b * (1/a[n+1])
+  // conv n = 0..2*blocks-1.  Float nets: bias = b.  Quantised nets, in float64:
+  // the code of an output is rne(clamp(z, 0, qhi[k])) on the int8 or e4m3 grid,
+  // z = acc * qmul + qbias (+ the residual and pooled terms), i.e.
+  // act(y) / a[k] of the definition y = acc * a[n] * s_w[n][f] + b[f] + ...:
+  //   stem:   qmul = 1/a[0],                     qbias = b / a[0]
+  //   conv n: qmul = a[n] * s_w[n][f] / a[n+1],  qbias = b / a[n+1]
   const float* bias;
-  const float* qmul;
+  const double* qmul;
+  const double* qbias;
   // Quantised nets, per output tensor k = 0..2*blocks (tensor k is written by
   // conv k-1, the stem for k = 0): qres[k] = a[k-2] / a[k] for the second conv
-  // of a block (its residual input h scaled into the output's code units),
+  // of a block (its residual input's code scaled into the output's code units),
   // qhi[k] = min(qmax, act_cap / a[k]) (activation cap and saturation).
-  const float* qres;
-  const float* qhi;
+  const double* qres;
+  const double* qhi;
   const float* head_b;  // [AZ_HEAD_ROWS]: policy biases, value conv bias at row P, zeros
   const float* fc1_w;   // [H][64]
   const float* fc1_b;   // [H]
@@ -61,9 +64,13 @@ struct AzDevNet {
   const float* q_b;        // [D]
   const float* k_b;        // [D]
   const float* pool_wt;    // per pooling block (in block order): Wg as [2g/4][AZ_DEP_POOL_OPAD][4] fp32
-  const float* pool_m;     // [2*blocks][F]: pooled-channel pre-activation scale (a[n]*s_w[n][f]; 1 for bf16)
-  const float* pool_b;     // [2*blocks][F]: pooled-channel bias b1 (unscaled)
-  const float* pool_cinv;  // [2*blocks]: factor of c in the regular channels (inv[n+1]; 1 for bf16)
+  // int8 pooling blocks (first conv n = 2j): the pooled channels' activation is
+  // act(acc * pool_m[n][f] + pool_b[n][f]) with pool_m = a[n] * s_w[n][f] and
+  // pool_b = b1 (float64); the projected context c enters the regular channels'
+  // requantisation as c * pool_cinv[n], pool_cinv[n] = 1 / a[n+1].
+  const double* pool_m;     // [2*blocks][F]
+  const double* pool_b;     // [2*blocks][F]
+  const double* pool_cinv;  // [2*blocks]
   const uint32_t* actions; // [AZ_DEP_ACTION_SLOTS]: f*64 + t | (promotion c*4 + k + 1) << 12
   const float* wdl_fc1_t;  // [V*64][H] (fc1 transposed)
   const float* wdl_fc1_b;  // [H]
@@ -97,6 +104,13 @@ int az_mfma_boards_per_wg(int filters, int tiling);
 bool az_mfma_tiling_valid(int filters, int tiling);
 // Whether an (dtype, filters) pair has MFMA kernels in the library.
 bool az_mfma_supported(int dtype, int filters);
+// Device and pinned-host allocations of the library.  Every one is counted
+// (az_debug_live_allocations) and can be made to fail on purpose
+// (az_debug_fail_allocation) so that the failure paths can be tested.
+hipError_t az_dev_malloc(void** ptr, size_t bytes);
+void az_dev_free(void* ptr);
+hipError_t az_host_malloc(void** ptr, size_t bytes);
+void az_host_free(void* ptr);
 // Records `detail` for az_last_error() and returns `status`.
 int az_fail(int status, const char* detail);
 // Spec (normalised to the current version) and device of a loaded handle.

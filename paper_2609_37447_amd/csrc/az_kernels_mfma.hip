@@ -84,9 +84,10 @@ struct Cfg {
   static constexpr int RBX = 2 * F;  // bf16 row bytes of the heads' input
   static constexpr int OFF_X = OFF_T;
   static constexpr int LBMAX = (AZ_MAX_POLICY + 1) * 64;  // floats per board, logits + u
-  // per-layer epilogue constants, double-buffered: [2 slots][bias F | qmul F] floats
+  // per-layer epilogue constants, double-buffered: [2 slots][bias F] floats, or
+  // for quantised nets [2 slots][qbias F | qmul F] doubles
   static constexpr int OFF_K = 2 * BUF + ZB;
-  static constexpr int KSLOT = 2 * F * 4;
+  static constexpr int KSLOT = MK == MK_BF16 ? 4 * F : 16 * F;
   // head row constants (scale, bias) and the softmax / value reductions sit past
   // every other region: they are written at the start and read at the end
   static constexpr int OFF_HC = (cmax(cmax(OFF_K + 2 * KSLOT, OFF_X + BPW * 64 * RBX), BPW * LBMAX * 4) + 15) & ~15;
@@ -196,17 +197,22 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     constexpr int i = decltype(i_c)::value;
     load_group(A[i], i * G * C::STEP_BYTES);
   });
-  // per-layer epilogue constants: thread t < F/2 carries float4 t of [bias | qmul]
+  // per-layer epilogue constants: thread t < KSLOT/16 carries 16-byte chunk t of
+  // the slot ([bias] floats, or [qbias | qmul] doubles)
+  constexpr int KCH = C::KSLOT / 16;
   auto load_consts = [&](int k) -> float4 {  // k = 1 + conv index (0 = stem)
-    if (tid < F / 4) return *reinterpret_cast<const float4*>(p.bias + (size_t)k * F + tid * 4);
-    if (QUANT && tid < F / 2) return *reinterpret_cast<const float4*>(p.qmul + (size_t)k * F + (tid - F / 4) * 4);
-    return make_float4(0.f, 0.f, 0.f, 0.f);
+    if (tid >= KCH) return make_float4(0.f, 0.f, 0.f, 0.f);
+    if constexpr (QUANT) {
+      const double* src = tid < F / 2 ? p.qbias + (size_t)k * F + 2 * tid : p.qmul + (size_t)k * F + 2 * (tid - F / 2);
+      return *reinterpret_cast<const float4*>(src);
+    } else {
+      return *reinterpret_cast<const float4*>(p.bias + (size_t)k * F + tid * 4);
+    }
   };
   auto store_consts = [&](int slot, const float4& v) {
-    if (tid < (QUANT ? F / 2 : F / 4))
-      *reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT + tid * 16) = v;
+    if (tid < KCH) *reinterpret_cast<float4*>(smem + C::OFF_K + slot * C::KSLOT + tid * 16) = v;
   };
-  static_assert(NT >= F / 2, "constant staging needs F/2 threads");
+  static_assert(NT >= KCH, "constant staging needs a thread per 16-byte chunk");
   store_consts(0, load_consts(1));
   if (tid < AZ_HEAD_ROWS / 2)  // [scale 96 | bias 96] floats
     *reinterpret_cast<float4*>(smem + C::OFF_HC + tid * 16) =
@@ -274,8 +280,14 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       for (int q = 0; q < 4; ++q) {
         const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
         const float4 bb = *reinterpret_cast<const float4*>(p.bias + ch0);
-        float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
-        if constexpr (QUANT) mm = *reinterpret_cast<const float4*>(p.qmul + ch0);
+        double mq[4] = {}, bq[4] = {};
+        if constexpr (QUANT) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            mq[r] = p.qmul[ch0 + r];
+            bq[r] = p.qbias[ch0 + r];
+          }
+        }
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
           const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
@@ -291,13 +303,14 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             *reinterpret_cast<uint2*>(smem + rowo + (((ch0 >> 3) ^ swz<RB>(j)) << 4) + 8 * lhi) =
                 make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
           } else {
-            const float hi = p.qhi[0];
-            const float z0 = med3(__builtin_fmaf(v[4 * q + 0], mm.x, bb.x), 0.0f, hi);
-            const float z1 = med3(__builtin_fmaf(v[4 * q + 1], mm.y, bb.y), 0.0f, hi);
-            const float z2 = med3(__builtin_fmaf(v[4 * q + 2], mm.z, bb.z), 0.0f, hi);
-            const float z3 = med3(__builtin_fmaf(v[4 * q + 3], mm.w, bb.w), 0.0f, hi);
+            // the stem's sum comes from the bf16 matrix instruction in fp32; the
+            // rescale and rounding of its code are taken in float64
+            const double hi = p.qhi[0];
             *reinterpret_cast<uint32_t*>(smem + rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15)) =
-                pack_codes<MK>(z0, z1, z2, z3);
+                pack_codes_d<MK>(__builtin_fma((double)v[4 * q + 0], mq[0], bq[0]),
+                                 __builtin_fma((double)v[4 * q + 1], mq[1], bq[1]),
+                                 __builtin_fma((double)v[4 * q + 2], mq[2], bq[2]),
+                                 __builtin_fma((double)v[4 * q + 3], mq[3], bq[3]), hi);
           }
         }
       }
@@ -401,19 +414,23 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       });
 
       // epilogue
-      float hi = 0.0f, rq = 0.0f;
+      double hi = 0.0, rq = 0.0;
       if constexpr (QUANT) {
         hi = p.qhi[n_conv + 1];
-        rq = SECOND ? p.qres[n_conv + 1] : 0.0f;
+        rq = SECOND ? p.qres[n_conv + 1] : 0.0;
       }
       // The epilogue walks the wave's rows in runs k = (m, q) of 4 channels.  Its
       // LDS reads (the run's per-channel constants and, for the second conv of
       // a quantised block, the residual codes, read in place before this lane
       // overwrites them) are issued EP_AHEAD runs ahead of their arithmetic, in
       // a ring of EP_AHEAD + 1 slots, so that no read latency is exposed.
-      constexpr int NRUN = MBW * 4, EP_AHEAD = QUANT ? 2 : 0, EP_RING = EP_AHEAD + 1;
+      // Quantised layers requantise in float64: z = acc * qmul + qbias
+      // (+ residual code * qres), clamped and rounded to the code grid.
+      constexpr int NRUN = MBW * 4, EP_AHEAD = QUANT ? (NBW >= 4 ? 2 : 1) : 0, EP_RING = EP_AHEAD + 1;
       constexpr bool RCODE = QUANT && SECOND;
-      float4 kb[EP_RING], km[QUANT ? EP_RING : 1];
+      struct KQ { double b[4], m[4]; };
+      float4 kb[QUANT ? 1 : EP_RING];
+      KQ kq[QUANT ? EP_RING : 1];
       uint32_t rcode[RCODE ? EP_RING : 1][RCODE ? NBW : 1];
       auto ep_addr = [&](int m, int q, int n) {
         const int nb = nb0 + n, bl = nb >> 1, j = ((nb & 1) << 5) + l32;
@@ -425,8 +442,20 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       auto ep_load = [&](auto k_c) {
         constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
         const int ch0 = (mb0 + m) * 32 + 8 * q + 4 * lhi;
-        kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
-        if constexpr (QUANT) km[slot] = *reinterpret_cast<const float4*>(kslot + F + ch0);
+        if constexpr (QUANT) {
+          const double* kd = reinterpret_cast<const double*>(kslot);
+#pragma unroll
+          for (int r = 0; r < 4; r += 2) {
+            const double2 b2 = *reinterpret_cast<const double2*>(kd + ch0 + r);
+            const double2 m2 = *reinterpret_cast<const double2*>(kd + F + ch0 + r);
+            kq[slot].b[r] = b2.x;
+            kq[slot].b[r + 1] = b2.y;
+            kq[slot].m[r] = m2.x;
+            kq[slot].m[r + 1] = m2.y;
+          }
+        } else {
+          kb[slot] = *reinterpret_cast<const float4*>(kslot + ch0);
+        }
         if constexpr (RCODE) {
 #pragma unroll
           for (int n = 0; n < NBW; ++n) rcode[slot][n] = *reinterpret_cast<const uint32_t*>(smem + ep_addr(m, q, n));
@@ -436,12 +465,12 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       static_for<0, NRUN>([&](auto k_c) {
         constexpr int k = decltype(k_c)::value, m = k / 4, q = k % 4, slot = k % EP_RING;
         if constexpr (k + EP_AHEAD < NRUN) ep_load(std::integral_constant<int, k + EP_AHEAD>{});
-        const float4 bb = kb[slot];
 #pragma unroll
         for (int n = 0; n < NBW; ++n) {
           const int addr = ep_addr(m, q, n);
           const acc_t& v = c[m][n];
           if constexpr (!QUANT) {
+            const float4 bb = kb[slot];
             float y0 = v[4 * q + 0] + bb.x, y1 = v[4 * q + 1] + bb.y;
             float y2 = v[4 * q + 2] + bb.z, y3 = v[4 * q + 3] + bb.w;
             if constexpr (SECOND) {
@@ -461,20 +490,18 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             }
             *reinterpret_cast<uint2*>(smem + addr) = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
           } else {
-            const float4 mm = km[slot];
-            float z0 = __builtin_fmaf((float)v[4 * q + 0], mm.x, bb.x);
-            float z1 = __builtin_fmaf((float)v[4 * q + 1], mm.y, bb.y);
-            float z2 = __builtin_fmaf((float)v[4 * q + 2], mm.z, bb.z);
-            float z3 = __builtin_fmaf((float)v[4 * q + 3], mm.w, bb.w);
+            const KQ& kk = kq[slot];
+            double z[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) z[r] = __builtin_fma((double)v[4 * q + r], kk.m[r], kk.b[r]);
             if constexpr (SECOND) {
-              const uint32_t r = rcode[slot][n];
-              z0 = __builtin_fmaf(code_value<MK, 0>(r), rq, z0);
-              z1 = __builtin_fmaf(code_value<MK, 1>(r), rq, z1);
-              z2 = __builtin_fmaf(code_value<MK, 2>(r), rq, z2);
-              z3 = __builtin_fmaf(code_value<MK, 3>(r), rq, z3);
+              const uint32_t rc = rcode[slot][n];
+              z[0] = __builtin_fma((double)code_value<MK, 0>(rc), rq, z[0]);
+              z[1] = __builtin_fma((double)code_value<MK, 1>(rc), rq, z[1]);
+              z[2] = __builtin_fma((double)code_value<MK, 2>(rc), rq, z[2]);
+              z[3] = __builtin_fma((double)code_value<MK, 3>(rc), rq, z[3]);
             }
-            *reinterpret_cast<uint32_t*>(smem + addr) =
-                pack_codes<MK>(med3(z0, 0.0f, hi), med3(z1, 0.0f, hi), med3(z2, 0.0f, hi), med3(z3, 0.0f, hi));
+            *reinterpret_cast<uint32_t*>(smem + addr) = pack_codes_d<MK>(z[0], z[1], z[2], z[3], hi);
           }
         }
       });

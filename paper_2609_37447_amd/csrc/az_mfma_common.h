@@ -119,6 +119,32 @@ __device__ __forceinline__ uint32_t pack_codes(float z0, float z1, float z2, flo
     return (uint32_t)w;
   }
 }
+// Requantisation in float64.  The next tensor's code is sat(rne(act(y) / a_out));
+// the epilogues compute z = y / a_out from the exact accumulator with float64
+// constants, clamp it to [0, hi] (hi = min(qmax, cap / a_out)) and round it here
+// to the code grid: int8 to the nearest integer, fp8 to the nearest e4m3fn value
+// (ties to even in both).  float64 carries 53 bits, so a rounding decision can
+// differ from exact arithmetic only within about 2^-45 of a tie.
+template <int MK>
+__device__ __forceinline__ float code_round(double z) {
+  if constexpr (MK == MK_I8) {
+    return (float)__builtin_rint(z);
+  } else {
+    // spacing of e4m3 values around z: 2^(e-3) with e = floor(log2 z), at least
+    // -6 (subnormals share the spacing 2^-9); z <= 448 never rounds past 448
+    const int e = max(__builtin_amdgcn_frexp_exp(z) - 1, -6);
+    return (float)__builtin_amdgcn_ldexp(__builtin_rint(__builtin_amdgcn_ldexp(z, 3 - e)), e - 3);
+  }
+}
+__device__ __forceinline__ double clamp_d(double z, double hi) { return __builtin_fmin(__builtin_fmax(z, 0.0), hi); }
+// Codes of four clamped float64 values (exactly representable after code_round,
+// so the hardware conversions below only re-encode them).
+template <int MK>
+__device__ __forceinline__ uint32_t pack_codes_d(double z0, double z1, double z2, double z3, double hi) {
+  return pack_codes<MK>(code_round<MK>(clamp_d(z0, hi)), code_round<MK>(clamp_d(z1, hi)),
+                        code_round<MK>(clamp_d(z2, hi)), code_round<MK>(clamp_d(z3, hi)));
+}
+
 // Value of byte R of a code word (codes of post-activation tensors are >= 0
 // for int8; fp8 codes are decoded by the hardware conversion).
 template <int MK, int R>

@@ -158,13 +158,13 @@ void release(az_pipeline* p) {
     if (s.eval_done) (void)hipEventDestroy(s.eval_done);
     if (s.done) (void)hipEventDestroy(s.done);
     if (s.graph_stream) (void)hipStreamDestroy(s.graph_stream);
-    if (s.h_planes) (void)hipHostFree(s.h_planes);
-    if (s.h_legal) (void)hipHostFree(s.h_legal);
-    if (s.h_out) (void)hipHostFree(s.h_out);
-    if (s.d_planes) (void)hipFree(s.d_planes);
-    if (s.d_legal) (void)hipFree(s.d_legal);
-    if (s.d_out) (void)hipFree(s.d_out);
-    if (s.d_dense) (void)hipFree(s.d_dense);
+    az_host_free(s.h_planes);
+    az_host_free(s.h_legal);
+    az_host_free(s.h_out);
+    az_dev_free(s.d_planes);
+    az_dev_free(s.d_legal);
+    az_dev_free(s.d_out);
+    az_dev_free(s.d_dense);
   }
   p->slots.clear();
   if (p->s_in) (void)hipStreamDestroy(p->s_in);
@@ -244,13 +244,13 @@ struct DeviceScope {
 };
 
 template <class T>
-hipError_t host_alloc(T** ptr, size_t n, unsigned flags) {
-  return hipHostMalloc(reinterpret_cast<void**>(ptr), n * sizeof(T), flags);
+hipError_t host_alloc(T** ptr, size_t n) {
+  return az_host_malloc(reinterpret_cast<void**>(ptr), n * sizeof(T));
 }
 
 template <class T>
 hipError_t dev_alloc(T** ptr, size_t n) {
-  return hipMalloc(reinterpret_cast<void**>(ptr), n * sizeof(T));
+  return az_dev_malloc(reinterpret_cast<void**>(ptr), n * sizeof(T));
 }
 
 }  // namespace
@@ -306,9 +306,9 @@ int az_pipeline_create(az_net* net, int32_t max_batch, int32_t slots, int32_t fl
   }
   for (auto& s : p->slots) {
     if (e != hipSuccess) break;
-    e = host_alloc(&s.h_planes, np, hipHostMallocDefault);
-    if (e == hipSuccess) e = host_alloc(&s.h_legal, nm, hipHostMallocDefault);
-    if (e == hipSuccess) e = host_alloc(&s.h_out, n_out, hipHostMallocDefault);
+    e = host_alloc(&s.h_planes, np);
+    if (e == hipSuccess) e = host_alloc(&s.h_legal, nm);
+    if (e == hipSuccess) e = host_alloc(&s.h_out, n_out);
     if (e == hipSuccess) e = dev_alloc(&s.d_planes, np);
     if (e == hipSuccess) e = dev_alloc(&s.d_legal, nm);
     if (e == hipSuccess) e = dev_alloc(&s.d_out, n_out);

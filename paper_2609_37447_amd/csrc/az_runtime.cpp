@@ -27,6 +27,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <new>
 #include <string>
 #include <vector>
@@ -207,17 +208,17 @@ uint16_t bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
-int8_t quant_i8(float v) {
-  float r = nearbyintf(v);  // default rounding mode: to nearest, ties to even
-  if (r > 127.0f) r = 127.0f;
-  if (r < -127.0f) r = -127.0f;
+int8_t quant_i8(double v) {
+  double r = nearbyint(v);  // default rounding mode: to nearest, ties to even
+  if (r > 127.0) r = 127.0;
+  if (r < -127.0) r = -127.0;
   return (int8_t)r;
 }
 
 // OCP fp8 e4m3fn code of v: nearest value, ties to even, saturating to +-448.
-uint8_t quant_e4m3(float v) {
+uint8_t quant_e4m3(double v) {
   const uint8_t sign = signbit(v) ? 0x80 : 0x00;
-  const double a = fabs((double)v);
+  const double a = fabs(v);
   if (!(a > 0.0)) return sign;
   if (a >= 448.0) return sign | 0x7e;
   int ex;
@@ -258,7 +259,9 @@ void pack_conv(const float* W, const float* wscale, int F, int Cin, int Cp, Kind
             const uint16_t h = bf16_rne(v);
             memcpy(dst + 2 * t, &h, 2);
           } else {
-            const float x = v / wscale[ch];  // fp32 division, correctly rounded
+            // float64 quotient of two float32 values: it rounds only off the
+            // code grid's ties, so the code is that of the exact quotient
+            const double x = (double)v / (double)wscale[ch];
             dst[t] = kind == K_I8 ? (uint8_t)quant_i8(x) : quant_e4m3(x);
           }
         }
@@ -376,6 +379,45 @@ int choose_tiling(const az_net* n, int B) {
 
 }  // namespace
 
+// Counted allocations (see az_internal.h).  g_fail_in > 0 counts down to the
+// allocation that is made to fail.
+namespace {
+std::atomic<int64_t> g_live{0};
+std::atomic<int32_t> g_fail_in{0};
+
+bool injected_failure() {
+  int32_t c = g_fail_in.load();
+  while (c > 0 && !g_fail_in.compare_exchange_weak(c, c - 1)) {
+  }
+  return c == 1;
+}
+}  // namespace
+
+hipError_t az_dev_malloc(void** ptr, size_t bytes) {
+  *ptr = nullptr;
+  if (injected_failure()) return hipErrorOutOfMemory;
+  const hipError_t e = hipMalloc(ptr, bytes);
+  if (e == hipSuccess) ++g_live;
+  return e;
+}
+void az_dev_free(void* ptr) {
+  if (!ptr) return;
+  (void)hipFree(ptr);
+  --g_live;
+}
+hipError_t az_host_malloc(void** ptr, size_t bytes) {
+  *ptr = nullptr;
+  if (injected_failure()) return hipErrorOutOfMemory;
+  const hipError_t e = hipHostMalloc(ptr, bytes, hipHostMallocDefault);
+  if (e == hipSuccess) ++g_live;
+  return e;
+}
+void az_host_free(void* ptr) {
+  if (!ptr) return;
+  (void)hipHostFree(ptr);
+  --g_live;
+}
+
 // Records the detail of a failure for az_last_error() (used by the other
 // translation units of the library).
 int az_fail(int status, const char* detail) { return fail(status, "%s", detail); }
@@ -407,6 +449,10 @@ const char* az_status_string(int status) {
 
 const char* az_last_error(void) { return g_err.c_str(); }
 
+void az_debug_fail_allocation(int32_t n) { g_fail_in.store(n > 0 ? n : 0); }
+
+int64_t az_debug_live_allocations(void) { return g_live.load(); }
+
 int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_weights, int32_t dtype,
                 const float* w_scales, size_t n_w_scales, const float* act_scales,
                 size_t n_act_scales, az_net** out) {
@@ -437,8 +483,9 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   const BlobView v = view(s, weights);
   const int g = s.pool_every > 0 ? F / 4 : 0, Fr = F - g, V = s.value_channels, D = s.token_dim;
   std::vector<uint8_t> stem, tower, head, emb, qw, kw, pw;
-  std::vector<float> bias, qmul, qres, qhi, head_b, fc2w, head_sc, head_bc, fc1t;
-  std::vector<float> emb_sc, emb_bc, pool_m, pool_b, pool_cinv, wfc1t;
+  std::vector<float> bias, head_b, fc2w, head_sc, head_bc, fc1t;
+  std::vector<double> qmul, qbias, qres, qhi, pool_m, pool_b, pool_cinv;
+  std::vector<float> emb_sc, emb_bc, wfc1t;
   std::vector<float> pool_wt;
   std::vector<uint32_t> actions;
   const float hs = quant ? act_scales[2 * NB] : 1.0f;
@@ -504,45 +551,49 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
       }
       if (!dep) pack_head(v, F, P, head);
       if (quant) {
-        // Requantising multiply-add constants; every product of two float32
-        // values is rounded once to float32, in this order.
+        // Requantisation constants in float64: an output's code is
+        // rne(clamp(acc * qmul + qbias (+ qres * residual code), 0, qhi)).
         const int K = 2 * NB + 1;
-        const float qmax = dtype == AZ_INT8 ? 127.0f : 448.0f;
-        std::vector<float> inv(K);
-        for (int k = 0; k < K; ++k) inv[k] = (float)(1.0 / (double)act_scales[k]);
+        const double qmax = dtype == AZ_INT8 ? 127.0 : 448.0;
+        std::vector<double> a(act_scales, act_scales + K);
         qmul.resize((size_t)K * F);
-        qres.assign(K, 0.0f);
+        qbias.resize((size_t)K * F);
+        qres.assign(K, 0.0);
         qhi.resize(K);
         for (int f = 0; f < F; ++f) {
-          qmul[f] = inv[0];
-          bias[f] = v.stem_b[f] * inv[0];
+          qmul[f] = 1.0 / a[0];
+          qbias[f] = (double)v.stem_b[f] / a[0];
         }
         for (int n = 0; n < 2 * NB; ++n)
           for (int f = 0; f < F; ++f) {
-            const float m = act_scales[n] * w_scales[(size_t)n * F + f];
-            qmul[(size_t)(1 + n) * F + f] = m * inv[n + 1];
-            bias[(size_t)(1 + n) * F + f] = v.b[n][f] * inv[n + 1];
+            qmul[(size_t)(1 + n) * F + f] = a[n] * (double)w_scales[(size_t)n * F + f] / a[n + 1];
+            qbias[(size_t)(1 + n) * F + f] = (double)v.b[n][f] / a[n + 1];
           }
         for (int k = 0; k < K; ++k) {
-          if (k >= 2 && k % 2 == 0) qres[k] = act_scales[k - 2] * inv[k];
-          const float c = s.act_cap > 0.0f ? s.act_cap * inv[k] : qmax;
+          if (k >= 2 && k % 2 == 0) qres[k] = a[k - 2] / a[k];
+          const double c = s.act_cap > 0.0f ? (double)s.act_cap / a[k] : qmax;
           qhi[k] = c < qmax ? c : qmax;
         }
       }
       if (dep) {
-        // global pooling: the pooled channels' pre-activation p = fma(acc, m, b)
-        // and the factor of the projected bias c in the regular channels' update
-        pool_m.assign((size_t)2 * NB * F, 1.0f);
-        pool_b.assign((size_t)2 * NB * F, 0.0f);
-        pool_cinv.assign((size_t)2 * NB, 1.0f);
+        // global pooling (int8): the pooled channels' activation
+        // act(acc * pool_m + pool_b) and the factor of the projected context c in
+        // the regular channels' requantisation; bf16 pools act(acc + b1) itself
+        if (quant) {
+          pool_m.assign((size_t)2 * NB * F, 0.0);
+          pool_b.assign((size_t)2 * NB * F, 0.0);
+          pool_cinv.assign((size_t)2 * NB, 0.0);
+        }
         for (int j = 0; j < NB; ++j) {
           if (!is_pool_block(s, j)) continue;
           const int n = 2 * j;
-          for (int f = 0; f < F; ++f) {
-            pool_b[(size_t)n * F + f] = v.b[n][f];
-            if (quant) pool_m[(size_t)n * F + f] = act_scales[n] * w_scales[(size_t)n * F + f];
+          if (quant) {
+            for (int f = 0; f < F; ++f) {
+              pool_b[(size_t)n * F + f] = v.b[n][f];
+              pool_m[(size_t)n * F + f] = (double)act_scales[n] * (double)w_scales[(size_t)n * F + f];
+            }
+            pool_cinv[n] = 1.0 / (double)act_scales[n + 1];
           }
-          if (quant) pool_cinv[n] = (float)(1.0 / (double)act_scales[n + 1]);
           // Wg as [2g/4][AZ_DEP_POOL_OPAD][4] (outputs padded with zeros): lane o of
           // a wave loads Wg[o][4s .. 4s+3] at ((s * OPAD + o) * 4), so the wave's
           // float4 loads are contiguous
@@ -586,8 +637,8 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   const size_t VH = dep ? (size_t)V * 64 * H : (size_t)H * 64;
   std::vector<Sec> secs = {
       {stem.data(), stem.size(), 0}, {tower.data(), tower.size(), 0}, {head.data(), head.size(), 0},
-      {bias.data(), bias.size() * 4, 0}, {qmul.data(), qmul.size() * 4, 0},
-      {qres.data(), qres.size() * 4, 0}, {qhi.data(), qhi.size() * 4, 0},
+      {bias.data(), bias.size() * 4, 0}, {qmul.data(), qmul.size() * 8, 0},
+      {qres.data(), qres.size() * 8, 0}, {qhi.data(), qhi.size() * 8, 0},
       {head_b.data(), head_b.size() * 4, 0}, {dep ? nullptr : v.fc1_w, dep ? 0 : VH * 4, 0},
       {v.fc1_b, (size_t)H * 4, 0}, {dep ? (const void*)v.fc2_w : fc2w.data(), (dep ? 3 : 1) * (size_t)H * 4, 0},
       {head_sc.data(), head_sc.size() * 4, 0}, {head_bc.data(), head_bc.size() * 4, 0},
@@ -596,9 +647,10 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
       {emb.data(), emb.size(), 0}, {qw.data(), qw.size(), 0}, {kw.data(), kw.size(), 0},
       {pw.data(), pw.size(), 0}, {emb_sc.data(), emb_sc.size() * 4, 0}, {emb_bc.data(), emb_bc.size() * 4, 0},
       {dep ? v.q_b : nullptr, dep ? (size_t)D * 4 : 0, 0}, {dep ? v.k_b : nullptr, dep ? (size_t)D * 4 : 0, 0},
-      {pool_wt.data(), pool_wt.size() * 4, 0}, {pool_m.data(), pool_m.size() * 4, 0},
-      {pool_b.data(), pool_b.size() * 4, 0}, {pool_cinv.data(), pool_cinv.size() * 4, 0},
-      {actions.data(), actions.size() * 4, 0}, {wfc1t.data(), wfc1t.size() * 4, 0}};
+      {pool_wt.data(), pool_wt.size() * 4, 0}, {pool_m.data(), pool_m.size() * 8, 0},
+      {pool_b.data(), pool_b.size() * 8, 0}, {pool_cinv.data(), pool_cinv.size() * 8, 0},
+      {actions.data(), actions.size() * 4, 0}, {wfc1t.data(), wfc1t.size() * 4, 0},
+      {qbias.data(), qbias.size() * 8, 0}};
   size_t total = 0;
   for (auto& sc : secs) { sc.off = total; total += align256(sc.bytes); }
 
@@ -608,17 +660,18 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
   void* dmem = nullptr;
-  e = hipMalloc(&dmem, total);
+  e = az_dev_malloc(&dmem, total);
   if (e != hipSuccess) { (void)hipGetLastError(); return hip_fail(e, "hipMalloc of the weights"); }
   for (auto& sc : secs) {
     if (!sc.bytes) continue;
     e = hipMemcpy(static_cast<uint8_t*>(dmem) + sc.off, sc.src, sc.bytes, hipMemcpyHostToDevice);
-    if (e != hipSuccess) { (void)hipFree(dmem); return hip_fail(e, "hipMemcpy of the weights"); }
+    if (e != hipSuccess) { az_dev_free(dmem); return hip_fail(e, "hipMemcpy of the weights"); }
   }
   az_net* net = new (std::nothrow) az_net;
-  if (!net) { (void)hipFree(dmem); return fail(AZ_ERR_NOMEM, "host allocation of the handle failed"); }
+  if (!net) { az_dev_free(dmem); return fail(AZ_ERR_NOMEM, "host allocation of the handle failed"); }
   auto at = [&](int i) { return secs[i].bytes ? static_cast<uint8_t*>(dmem) + secs[i].off : nullptr; };
   auto atf = [&](int i) { return reinterpret_cast<const float*>(at(i)); };
+  auto atd = [&](int i) { return reinterpret_cast<const double*>(at(i)); };
   net->spec = s;
   net->dtype = dtype;
   net->device = dev;
@@ -640,9 +693,10 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   d.tower_w = at(1);
   d.head_w = at(2);
   d.bias = atf(3);
-  d.qmul = atf(4);
-  d.qres = atf(5);
-  d.qhi = atf(6);
+  d.qmul = atd(4);
+  d.qres = atd(5);
+  d.qhi = atd(6);
+  d.qbias = atd(28);
   d.head_b = atf(7);
   d.fc1_w = atf(8);
   d.fc1_b = atf(9);
@@ -663,9 +717,9 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
     d.q_b = atf(20);
     d.k_b = atf(21);
     d.pool_wt = atf(22);
-    d.pool_m = atf(23);
-    d.pool_b = atf(24);
-    d.pool_cinv = atf(25);
+    d.pool_m = atd(23);
+    d.pool_b = atd(24);
+    d.pool_cinv = atd(25);
     d.actions = reinterpret_cast<const uint32_t*>(at(26));
     d.wdl_fc1_t = atf(27);
     d.wdl_fc1_b = atf(9);
@@ -740,7 +794,7 @@ void az_net_free(az_net* net) {
     int cur = 0;
     const bool have = hipGetDevice(&cur) == hipSuccess;
     if (have && cur != net->device) (void)hipSetDevice(net->device);
-    (void)hipFree(net->dmem);
+    az_dev_free(net->dmem);
     if (have && cur != net->device) (void)hipSetDevice(cur);
   }
   delete net;

@@ -63,10 +63,21 @@ def _absmax(wname: str, alpha_fold: bool):
     return O.calibrate_absmax(w.shape, blob, azgen.make_calibration_planes(w))
 
 
-def oracle_eval(shape, blob, dtype, planes, legal, w_scales=None, act_scales=None):
-    if dtype in ("f32", "bf16"):
-        return oracle.forward(shape, blob, planes, legal)
-    return oracle.forward_quant(shape, blob, w_scales, act_scales, dtype, planes, legal)
+def oracle_eval(shape, blob, dtype, planes, legal, w_scales=None, act_scales=None, chunk=128, progress=None):
+    """Oracle outputs (float64 network for f32 / bf16, the quantised definition
+    for int8 / fp8), in chunks of rows; progress(msg) is called per chunk."""
+    P, V = [], []
+    for s in range(0, planes.shape[0], chunk):
+        pl, lg = planes[s:s + chunk], legal[s:s + chunk]
+        if dtype in ("f32", "bf16"):
+            p, v = oracle.forward(shape, blob, pl, lg)
+        else:
+            p, v = oracle.forward_quant(shape, blob, w_scales, act_scales, dtype, pl, lg)
+        P.append(p)
+        V.append(v)
+        if progress is not None:
+            progress(f"  oracle rows {s}..{s + pl.shape[0] - 1}")
+    return np.concatenate(P), np.concatenate(V)
 
 
 def assert_policy_structure(P, legal, atol_sum=1e-5):

@@ -4,7 +4,12 @@ ABI on seeded inputs.
 
 int8 (the paper's deployment: int8 trunk with the fixed ReLU6 activation scale
 6/127, per-output-channel weight scales, pooling and heads in floating point)
-is compared with the oracle's int8 network; bf16 with the float64 network.
+is compared with the oracle's int8 network, the plain float64 definition
+(exact integer sums, float64 pooling, rescale and rounding); bf16 with the
+float64 network.  The kernels compute the same definition except for the bf16
+stem's fp32 sums: on the CPU that flips 1 of the 10.5 M stem codes of the
+seeded 1,024-position batch, which moves that position by max|dP| 0.0044 and
+|dV| 0.0098, under a third of the tolerance.
 Tolerances: int8 max |dP| 3e-2 and |dV| 5e-2, bf16 1e-2 and 2e-2 (the WDL
 probabilities are held to the value tolerance).  Both kernel tilings (one wave
 per board, four waves per board) are run and must agree bitwise."""
@@ -160,31 +165,39 @@ def test_deployed_pooling_period(pool_every, dtype, tiling):
     _check(got, ref, legal, dtype)
 
 
-def test_deployed_14x160_int8_batch1024_sampled_rows():
+def _oracle_rows(shape, blob, dtype, planes, legal, ws, acs, chunk=128):
+    outs = []
+    for s in range(0, planes.shape[0], chunk):
+        pl, lg = planes[s:s + chunk], legal[s:s + chunk]
+        outs.append(OD.forward_quant(shape, blob, ws, acs, pl, lg) if dtype == "int8"
+                    else OD.forward(shape, blob, pl, lg))
+        print(f"  oracle rows {s}..{s + pl.shape[0] - 1}", flush=True)
+    return tuple(np.concatenate([o[i] for o in outs]) for i in range(3))
+
+
+def test_deployed_14x160_int8_batch1024_every_row():
     w = azgen.WORKLOADS["deployed14x160_int8_b1024"]
     blob = azgen.workload_weights(w)
     planes, legal = azgen.make_inputs(w)
     ws, acs = _scales(w.shape, blob)
     Pg, Vg, Wg = gpu_eval(w.shape, blob, "int8", planes, legal, ws, acs)
     assert_policy_structure(Pg, legal)
-    rows = np.r_[0:24, 500:508, 1000:1024]
-    ref = OD.forward_quant(w.shape, blob, ws, acs, planes[rows], legal[rows])
-    _check((Pg[rows], Vg[rows], Wg[rows]), ref, legal[rows], "int8")
+    ref = _oracle_rows(w.shape, blob, "int8", planes, legal, ws, acs)
+    _check((Pg, Vg, Wg), ref, legal, "int8")
 
 
-def test_deployed_14x160_bf16_sampled_rows():
+def test_deployed_14x160_bf16_every_row():
     w = azgen.WORKLOADS["deployed14x160_bf16_b1024"]
     blob = azgen.workload_weights(w)
     planes, legal = azgen.make_inputs(w, n=256)
     Pg, Vg, Wg = gpu_eval(w.shape, blob, "bf16", planes, legal)
     assert_policy_structure(Pg, legal)
-    rows = np.r_[0:16, 240:256]
-    ref = OD.forward(w.shape, blob, planes[rows], legal[rows])
-    _check((Pg[rows], Vg[rows], Wg[rows]), ref, legal[rows], "bf16")
+    ref = _oracle_rows(w.shape, blob, "bf16", planes, legal, None, None)
+    _check((Pg, Vg, Wg), ref, legal, "bf16")
 
 
 @pytest.mark.parametrize("dtype,B", [("int8", 64), ("int8", 256), ("bf16", 64)])
-def test_deployed_14x160_small_batch_sampled_rows(dtype, B):
+def test_deployed_14x160_small_batch_every_row(dtype, B):
     # the interactive regime: the default tiling below 257 boards is four waves per board
     w = azgen.WORKLOADS[f"deployed14x160_{dtype}_b1024"]
     blob = azgen.workload_weights(w)
@@ -192,10 +205,8 @@ def test_deployed_14x160_small_batch_sampled_rows(dtype, B):
     ws, acs = _scales(w.shape, blob) if dtype == "int8" else (None, None)
     Pg, Vg, Wg = gpu_eval(w.shape, blob, dtype, planes, legal, ws, acs)
     assert_policy_structure(Pg, legal)
-    rows = np.r_[0:8, B - 8:B]
-    ref = (OD.forward_quant(w.shape, blob, ws, acs, planes[rows], legal[rows]) if dtype == "int8"
-           else OD.forward(w.shape, blob, planes[rows], legal[rows]))
-    _check((Pg[rows], Vg[rows], Wg[rows]), ref, legal[rows], dtype)
+    ref = _oracle_rows(w.shape, blob, dtype, planes, legal, ws, acs)
+    _check((Pg, Vg, Wg), ref, legal, dtype)
 
 
 @pytest.mark.parametrize("dtype", ["int8", "bf16"])
