@@ -155,20 +155,32 @@ def cpu_baseline(w, blob, ws, acs, planes, legal, budget_s=12.0, chunk=64):
             break
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": done / el, "unit": "positions/s", "cores": int(threads), "kind": "oracle",
+            "host_cores": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
             "sample": f"{done} positions of the seeded batch in chunks of {chunk}, "
-                      f"{el:.1f} s, float64 numpy/BLAS"
-                      + (f" ({w.dtype} quantised network)" if w.dtype in ("int8", "fp8") else "")}
+                      f"{el:.1f} s, float64 numpy/BLAS on {threads} threads"
+                      + (f" ({w.dtype} quantised network, the plain definition)" if w.dtype in ("int8", "fp8") else "")}
 
 
-def pipeline_rates(az, net, w, planes, legal, steps, max_legal=256):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def pipeline_rates(az, net, w, planes, legal, batches=100, warm=10, max_legal=256):
     """Positions/s through az_pipeline, host buffers to host buffers: inputs
     copied from pinned memory, evaluation, outputs back in host memory.  Worker
     threads share one pipeline; each owns some of its slots and keeps them in
     flight round-robin (wait for the slot, resubmit it).  Three set-ups: dense
     policy, one worker with four slots of the full batch; the same with the
     compact legal-move policy; and four workers with two outstanding batches of
-    320 each, compact.  Measured after the timed region; never the headline
-    value."""
+    320 each, compact.  Each worker runs `warm` batches untimed, then `batches`
+    timed ones.  Measured after the timed region; never the headline value."""
     import threading
 
     B = w.batch
@@ -177,7 +189,7 @@ def pipeline_rates(az, net, w, planes, legal, steps, max_legal=256):
            "bytes_in_per_position": int(planes[0].nbytes + legal[0].nbytes),
            "bytes_out_per_position_dense": int((n_moves + 1) * 4),
            "bytes_out_per_position_compact": int((max_legal + 2) * 4)}
-    n = max(8, min(steps, 100))
+    n = batches
     has = legal.any(axis=1)
     for name, workers, per_worker, batch, K in (("dense_1w4s_b%d" % B, 1, 4, B, 0),
                                                 ("compact_1w4s_b%d" % B, 1, 4, B, max_legal),
@@ -193,25 +205,34 @@ def pipeline_rates(az, net, w, planes, legal, steps, max_legal=256):
             for k in range(slots):
                 pipe.wait(k)
             go = threading.Barrier(workers + 1)
+            timed = threading.Barrier(workers + 1)
             errors = []
 
             def run(mine):
                 go.wait()
                 try:
-                    for i in range(n):
-                        k = mine[i % len(mine)]
-                        pipe.wait(k)
-                        pipe.submit(k, batch)
-                    for k in mine:
-                        pipe.wait(k)
+                    for phase, count in (("warm", warm), ("timed", n)):
+                        if phase == "timed":
+                            timed.wait()
+                        for i in range(count):
+                            k = mine[i % len(mine)]
+                            pipe.wait(k)
+                            pipe.submit(k, batch)
+                        for k in mine:
+                            pipe.wait(k)
                 except Exception as e:  # reported below
                     errors.append(e)
+                    timed.abort()
 
             th = [threading.Thread(target=run, args=(list(range(j * per_worker, (j + 1) * per_worker)),))
                   for j in range(workers)]
             for t in th:
                 t.start()
             go.wait()
+            try:
+                timed.wait()
+            except threading.BrokenBarrierError:
+                pass
             t0 = time.perf_counter()
             for t in th:
                 t.join()
@@ -223,7 +244,8 @@ def pipeline_rates(az, net, w, planes, legal, steps, max_legal=256):
             assert np.all(np.abs(v[2][:batch][has[:batch]].sum(axis=1) - 1.0) < 1e-3), "pipeline outputs invalid"
         finally:
             pipe.close()
-        res[name] = {"positions_per_s": workers * n * batch / dt, "batches": workers * n}
+        res[name] = {"positions_per_s": workers * n * batch / dt, "batches": workers * n,
+                     "warmup_batches": workers * warm}
     return res
 
 
@@ -242,6 +264,8 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay measurement")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the host-buffer (PCIe-inclusive) pipeline measurement")
+    ap.add_argument("--pipeline-batches", type=int, default=100,
+                    help="timed batches per worker in each pipeline set-up (after 10 untimed)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -330,7 +354,8 @@ def main():
         torch.cuda.synchronize()
         graph_us = g0.elapsed_time(g1) * 1000.0 / n_rep
         del g
-    pipeline = None if (args.no_pipeline or B != w.batch) else pipeline_rates(az, net, w, planes, legal, args.steps)
+    pipeline = None if (args.no_pipeline or B != w.batch) else pipeline_rates(az, net, w, planes, legal,
+                                                                               args.pipeline_batches)
     az.az_net_free(net)
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)
