@@ -109,9 +109,14 @@ __device__ __forceinline__ void wave_sync() {
 template <bool QUANT>
 __device__ __forceinline__ double2 pool_row(const AzDevNet& p, const float* pt, int pc, int n_conv) {
   double sum = 0.0, mx = 0.0;  // activations are >= 0
+  // values made opaque to the compiler so that they are formed here, in the
+  // pooling layer, not hoisted out of the block loop and held across the tower
+  asm volatile("" : "+v"(pc));
   if constexpr (QUANT) {
     const size_t o = (size_t)n_conv * DF + DFR + pc;
-    const double pm = p.pool_m[o], pb = p.pool_b[o], cap = p.act_cap;
+    double cap = p.act_cap;
+    asm volatile("" : "+v"(cap));
+    const double pm = p.pool_m[o], pb = p.pool_b[o];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int4 v = *reinterpret_cast<const int4*>(pt + pc * 64 + ((j ^ (pc & 15)) << 2));
@@ -266,12 +271,17 @@ __device__ __forceinline__ void dep_wdl(const AzDevNet& p, const float* U, float
 template <int MK>
 __device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, const uint8_t* __restrict__ legal,
                                           float* __restrict__ policy, float* __restrict__ value,
-                                          float* __restrict__ wdl, int b, int lane) {
+                                          float* __restrict__ wdl, int b, int lane_in) {
   using C = DepCfg<MK>;
   using R = Rot<C::RB>;
   using RX = Rot<C::RBX>;
   constexpr bool QUANT = C::QUANT;
   constexpr int RB = C::RB, OFF_H = C::OFF_H;
+  // the lane index, opaque to the compiler here, so that the heads' lane-dependent
+  // addresses are computed in the heads instead of being shared with the stem's
+  // and held (or spilled) across the tower
+  int lane = lane_in;
+  asm volatile("" : "+v"(lane));
   const int l32 = lane & 31, lhi = lane >> 5;
 
   // ---- embedding: E[row][sq] = sum_f Wemb[row][f] h[f][sq], rows = tokens then value channels
@@ -362,54 +372,73 @@ __device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, cons
     }
   }
 
-  // Operand fragments from accumulators: K step s of a 128-row accumulator
-  // set X[4][2] (rows = the product's K dimension) for column block n holds
-  // positions 8s .. 8s+7 of the lane's 64 accumulator values.
-  auto frags_of = [&](const f32x16(&X)[DTB][2], int n, int s, bf16x8& hi, bf16x8& lo) {
-    float x[8];
+  // The token values as split bf16 operand fragments: K step s (0..7) of the
+  // products below holds positions 8s .. 8s+7 of the lane's 64 token values
+  // (the accumulators' register order), as x = hi + lo.
+  bf16x8 tkh[DD / 16][2], tkl[DD / 16][2];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) x[t] = X[(8 * s + t) / 16][n][(8 * s + t) % 16];
-    split8(x, hi, lo);
+  for (int st = 0; st < DD / 16; ++st)
+#pragma unroll
+    for (int n = 0; n < 2; ++n) {
+      float x[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) x[t] = tok[(8 * st + t) / 16][n][(8 * st + t) % 16];
+      split8(x, tkh[st][n], tkl[st][n]);
+    }
+
+  // action table entries and legal-mask words of the softmax, in flight during
+  // the last query / key block's products
+  constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
+  uint4 tbl[NIT];
+  uint32_t mkw[NIT];
+  auto load_actions = [&]() {
+    const uint8_t* lg = legal + (size_t)b * NA;
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int a0 = 256 * i + 4 * lane;
+      const bool in = a0 < NA;
+      tbl[i] = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
+      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
+      mkw[i] = in ? mk0 : 0u;
+    }
   };
-  // Q^T = Wq tok^T + bq and K^T = Wk tok^T + bk in one pass over the token
-  // fragments (split operands); rows of Q^T and K^T in the token accumulators'
-  // register order, so the token values die as the pass ends
-  f32x16 Qa[DTB][2], Ka[DTB][2];
+
+  // Per 32-row block m of Q^T = Wq tok^T + bq and K^T = Wk tok^T + bk (rows in
+  // the token accumulators' register order), then the two K steps 2m, 2m+1 of
+  //   S[f][t] = sum_d Q[f][d] K[t][d]      (hi*hi + hi*lo + lo*hi)
+  //   O^T[k][t] = sum_d Wp[k][d] K[t][d]   (promotion offsets, last row's destinations)
+  // that block holds.  Every accumulator runs the same chain of products as
+  // when all blocks are computed at once (the four-wave heads do that), with
+  // only one block of Q and K live at a time.
+  f32x16 Sa[2][2], Oa;
   {
     const uint8_t* qp = static_cast<const uint8_t*>(p.q_w) + (size_t)lane * 16;
     const uint8_t* kp = static_cast<const uint8_t*>(p.k_w) + (size_t)lane * 16;
-    // A fragments of K step s in ring slot s % 2, loaded one step ahead
+    const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
     constexpr int QS = DD / 16, QR = 2;
-    bf16x8 aqr[QR][DTB], akr[QR][DTB];
-    auto load_qk = [&](int st) {
 #pragma unroll
-      for (int m = 0; m < DTB; ++m) {
-        aqr[st % QR][m] = g_frag<MK_BF16>(qp + (st * DTB + m) * 64 * 16);
-        akr[st % QR][m] = g_frag<MK_BF16>(kp + (st * DTB + m) * 64 * 16);
-      }
-    };
+    for (int m = 0; m < DTB; ++m) {
+      if (m == DTB - 1) load_actions();
+      const bf16x8 apw0 = g_frag<MK_BF16>(pw + (2 * m) * 64 * 16), apw1 = g_frag<MK_BF16>(pw + (2 * m + 1) * 64 * 16);
+      f32x16 Qm[2], Km[2];
+      // A fragments of K step s in ring slot s % 2, loaded one step ahead
+      bf16x8 aqr[QR], akr[QR];
+      auto load_qk = [&](int st) {
+        aqr[st % QR] = g_frag<MK_BF16>(qp + (st * DTB + m) * 64 * 16);
+        akr[st % QR] = g_frag<MK_BF16>(kp + (st * DTB + m) * 64 * 16);
+      };
+      load_qk(0);
 #pragma unroll
-    for (int st = 0; st < QR - 1; ++st) load_qk(st);
+      for (int st = 0; st < QS; ++st) {
+        if (st + 1 < QS) load_qk(st + 1);
 #pragma unroll
-    for (int s = 0; s < QS; ++s) {
-      if (s + QR - 1 < QS) load_qk(s + QR - 1);
-      const bf16x8(&aq)[DTB] = aqr[s % QR];
-      const bf16x8(&ak)[DTB] = akr[s % QR];
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        bf16x8 xh, xl;
-        frags_of(tok, n, s, xh, xl);
-#pragma unroll
-        for (int m = 0; m < DTB; ++m) {
-          Qa[m][n] = mma_bf16(aq[m], xh, s == 0 ? f32x16{} : Qa[m][n]);
-          Qa[m][n] = mma_bf16(aq[m], xl, Qa[m][n]);
-          Ka[m][n] = mma_bf16(ak[m], xh, s == 0 ? f32x16{} : Ka[m][n]);
-          Ka[m][n] = mma_bf16(ak[m], xl, Ka[m][n]);
+        for (int n = 0; n < 2; ++n) {
+          Qm[n] = mma_bf16(aqr[st % QR], tkh[st][n], st == 0 ? f32x16{} : Qm[n]);
+          Qm[n] = mma_bf16(aqr[st % QR], tkl[st][n], Qm[n]);
+          Km[n] = mma_bf16(akr[st % QR], tkh[st][n], st == 0 ? f32x16{} : Km[n]);
+          Km[n] = mma_bf16(akr[st % QR], tkl[st][n], Km[n]);
         }
       }
-    }
-#pragma unroll
-    for (int m = 0; m < DTB; ++m)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
         const int r0 = 32 * m + 8 * jq + 4 * lhi;
@@ -420,54 +449,36 @@ __device__ __forceinline__ void dep_heads(const AzDevNet& p, uint8_t* smem, cons
         for (int n = 0; n < 2; ++n)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            Qa[m][n][4 * jq + r] += qv[r];
-            Ka[m][n][4 * jq + r] += kv[r];
+            Qm[n][4 * jq + r] += qv[r];
+            Km[n][4 * jq + r] += kv[r];
           }
       }
-  }
-
-  // S[f][t] = sum_d Q[f][d] K[t][d] (hi*hi + hi*lo + lo*hi) and the promotion
-  // offsets O^T[k][t] = sum_d Wp[k][d] K[t][d] for the last row's destinations
-  // action table entries and legal-mask words of the softmax, in flight
-  // during the query-key products
-  constexpr int NA = AZ_FROMTO_ACTIONS, NIT = (NA + 255) / 256;
-  uint4 tbl[NIT];
-  uint32_t mkw[NIT];
-  {
-    const uint8_t* lg = legal + (size_t)b * NA;
 #pragma unroll
-    for (int i = 0; i < NIT; ++i) {
-      const int a0 = 256 * i + 4 * lane;
-      const bool in = a0 < NA;
-      tbl[i] = *reinterpret_cast<const uint4*>(p.actions + (in ? a0 : 0));
-      const uint32_t mk0 = *reinterpret_cast<const uint32_t*>(lg + (in ? a0 : 0));  // clamped, unconditional
-      mkw[i] = in ? mk0 : 0u;
-    }
-  }
-  f32x16 Sa[2][2], Oa;
-  {
-    const uint8_t* pw = static_cast<const uint8_t*>(p.p_w) + (size_t)lane * 16;
-    bf16x8 apw[DD / 16];  // every K step's promotion-weight fragment, loaded up front
+      for (int h = 0; h < 2; ++h) {
+        const int s = 2 * m + h;
+        bf16x8 qh[2], ql[2], kh[2], kl[2];
 #pragma unroll
-    for (int s = 0; s < DD / 16; ++s) apw[s] = g_frag<MK_BF16>(pw + s * 64 * 16);
+        for (int n = 0; n < 2; ++n) {
+          float xq[8], xk[8];
 #pragma unroll
-    for (int s = 0; s < DD / 16; ++s) {
-      bf16x8 qh[2], ql[2], kh[2], kl[2];
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        frags_of(Qa, n, s, qh[n], ql[n]);
-        frags_of(Ka, n, s, kh[n], kl[n]);
-      }
-#pragma unroll
-      for (int mf = 0; mf < 2; ++mf)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          Sa[mf][nt] = mma_bf16(qh[mf], kh[nt], s == 0 ? f32x16{} : Sa[mf][nt]);
-          Sa[mf][nt] = mma_bf16(qh[mf], kl[nt], Sa[mf][nt]);
-          Sa[mf][nt] = mma_bf16(ql[mf], kh[nt], Sa[mf][nt]);
+          for (int t = 0; t < 8; ++t) {
+            xq[t] = Qm[n][8 * h + t];
+            xk[t] = Km[n][8 * h + t];
+          }
+          split8(xq, qh[n], ql[n]);
+          split8(xk, kh[n], kl[n]);
         }
-      Oa = mma_bf16(apw[s], kh[1], s == 0 ? f32x16{} : Oa);
-      Oa = mma_bf16(apw[s], kl[1], Oa);
+#pragma unroll
+        for (int mf = 0; mf < 2; ++mf)
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt) {
+            Sa[mf][nt] = mma_bf16(qh[mf], kh[nt], s == 0 ? f32x16{} : Sa[mf][nt]);
+            Sa[mf][nt] = mma_bf16(qh[mf], kl[nt], Sa[mf][nt]);
+            Sa[mf][nt] = mma_bf16(ql[mf], kh[nt], Sa[mf][nt]);
+          }
+        Oa = mma_bf16(h ? apw1 : apw0, kh[1], s == 0 ? f32x16{} : Oa);
+        Oa = mma_bf16(h ? apw1 : apw0, kl[1], Oa);
+      }
     }
   }
   // logits pre-scaled by log2(e) for the exp2 softmax
@@ -1232,7 +1243,8 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
       // epilogue: per run of 4 channels; LDS reads of constants (and residual
       // codes) issued two runs ahead
-      double hi = 0.0, rq = 0.0;
+      float hi = 0.0f;
+      double rq = 0.0;
       if constexpr (QUANT) {
         hi = p.qhi[n_conv + 1];
         rq = SECOND ? p.qres[n_conv + 1] : 0.0;
@@ -1316,10 +1328,10 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             for (int r = 0; r < 4; ++r) z[r] = __builtin_fma((double)v[4 * q + r], kk.m[r], kk.b[r]);
             if constexpr (SECOND) {
               const uint32_t rc = rcode[slot][n];
-              z[0] = __builtin_fma((double)code_value<MK, 0>(rc), rq, z[0]);
-              z[1] = __builtin_fma((double)code_value<MK, 1>(rc), rq, z[1]);
-              z[2] = __builtin_fma((double)code_value<MK, 2>(rc), rq, z[2]);
-              z[3] = __builtin_fma((double)code_value<MK, 3>(rc), rq, z[3]);
+              z[0] = __builtin_fma(code_value_d<MK, 0>(rc), rq, z[0]);
+              z[1] = __builtin_fma(code_value_d<MK, 1>(rc), rq, z[1]);
+              z[2] = __builtin_fma(code_value_d<MK, 2>(rc), rq, z[2]);
+              z[3] = __builtin_fma(code_value_d<MK, 3>(rc), rq, z[3]);
             }
             *reinterpret_cast<uint32_t*>(smem + addr) = pack_codes_d<MK>(z[0], z[1], z[2], z[3], hi);
           }
@@ -1774,7 +1786,8 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
 
         // epilogue: per run of 4 channels; LDS reads of constants (and residual
         // codes) issued two runs ahead
-        double hi = 0.0, rq = 0.0;
+        float hi = 0.0f;
+        double rq = 0.0;
         if constexpr (QUANT) {
           hi = p.qhi[n_conv + 1];
           rq = SECOND ? p.qres[n_conv + 1] : 0.0;
@@ -1861,10 +1874,10 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
               for (int r = 0; r < 4; ++r) z[r] = __builtin_fma((double)v[4 * q + r], kk.m[r], kk.b[r]);
               if constexpr (SECOND) {
                 const uint32_t rc = rcode[slot][n];
-                z[0] = __builtin_fma((double)code_value<MK, 0>(rc), rq, z[0]);
-                z[1] = __builtin_fma((double)code_value<MK, 1>(rc), rq, z[1]);
-                z[2] = __builtin_fma((double)code_value<MK, 2>(rc), rq, z[2]);
-                z[3] = __builtin_fma((double)code_value<MK, 3>(rc), rq, z[3]);
+                z[0] = __builtin_fma(code_value_d<MK, 0>(rc), rq, z[0]);
+                z[1] = __builtin_fma(code_value_d<MK, 1>(rc), rq, z[1]);
+                z[2] = __builtin_fma(code_value_d<MK, 2>(rc), rq, z[2]);
+                z[3] = __builtin_fma(code_value_d<MK, 3>(rc), rq, z[3]);
               }
               *reinterpret_cast<uint32_t*>(smem + addr) = pack_codes_d<MK>(z[0], z[1], z[2], z[3], hi);
             }

@@ -37,9 +37,10 @@ struct AzDevNet {
   // Quantised nets, per output tensor k = 0..2*blocks (tensor k is written by
   // conv k-1, the stem for k = 0): qres[k] = a[k-2] / a[k] for the second conv
   // of a block (its residual input's code scaled into the output's code units),
-  // qhi[k] = min(qmax, act_cap / a[k]) (activation cap and saturation).
+  // qhi[k] = the largest code of tensor k, min(qmax, act_cap / a[k]) rounded to
+  // the code grid (activation cap and saturation).
   const double* qres;
-  const double* qhi;
+  const float* qhi;
   const float* head_b;  // [AZ_HEAD_ROWS]: policy biases, value conv bias at row P, zeros
   const float* fc1_w;   // [H][64]
   const float* fc1_b;   // [H]

@@ -305,7 +305,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           } else {
             // the stem's sum comes from the bf16 matrix instruction in fp32; the
             // rescale and rounding of its code are taken in float64
-            const double hi = p.qhi[0];
+            const float hi = p.qhi[0];
             *reinterpret_cast<uint32_t*>(smem + rowo + (((ch0 >> 4) ^ swz<RB>(j)) << 4) + (ch0 & 15)) =
                 pack_codes_d<MK>(__builtin_fma((double)v[4 * q + 0], mq[0], bq[0]),
                                  __builtin_fma((double)v[4 * q + 1], mq[1], bq[1]),
@@ -414,7 +414,8 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       });
 
       // epilogue
-      double hi = 0.0, rq = 0.0;
+      float hi = 0.0f;
+      double rq = 0.0;
       if constexpr (QUANT) {
         hi = p.qhi[n_conv + 1];
         rq = SECOND ? p.qres[n_conv + 1] : 0.0;
@@ -423,10 +424,12 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       // LDS reads (the run's per-channel constants and, for the second conv of
       // a quantised block, the residual codes, read in place before this lane
       // overwrites them) are issued EP_AHEAD runs ahead of their arithmetic, in
-      // a ring of EP_AHEAD + 1 slots, so that no read latency is exposed.
-      // Quantised layers requantise in float64: z = acc * qmul + qbias
-      // (+ residual code * qres), clamped and rounded to the code grid.
-      constexpr int NRUN = MBW * 4, EP_AHEAD = QUANT ? (NBW >= 4 ? 2 : 1) : 0, EP_RING = EP_AHEAD + 1;
+      // a ring of EP_AHEAD + 1 slots, so that no read latency is exposed (two
+      // runs in the four-board tiling, one in the two-board one; the one-board
+      // tiling has no registers to spare for the float64 constants and reads
+      // them in place).  Quantised layers requantise in float64: z = acc * qmul
+      // + qbias (+ residual code * qres), rounded to the code grid and clamped.
+      constexpr int NRUN = MBW * 4, EP_AHEAD = QUANT ? (NBW >= 4 ? 2 : (BPW == 1 ? 0 : 1)) : 0, EP_RING = EP_AHEAD + 1;
       constexpr bool RCODE = QUANT && SECOND;
       struct KQ { double b[4], m[4]; };
       float4 kb[QUANT ? 1 : EP_RING];
@@ -496,10 +499,10 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
             for (int r = 0; r < 4; ++r) z[r] = __builtin_fma((double)v[4 * q + r], kk.m[r], kk.b[r]);
             if constexpr (SECOND) {
               const uint32_t rc = rcode[slot][n];
-              z[0] = __builtin_fma((double)code_value<MK, 0>(rc), rq, z[0]);
-              z[1] = __builtin_fma((double)code_value<MK, 1>(rc), rq, z[1]);
-              z[2] = __builtin_fma((double)code_value<MK, 2>(rc), rq, z[2]);
-              z[3] = __builtin_fma((double)code_value<MK, 3>(rc), rq, z[3]);
+              z[0] = __builtin_fma(code_value_d<MK, 0>(rc), rq, z[0]);
+              z[1] = __builtin_fma(code_value_d<MK, 1>(rc), rq, z[1]);
+              z[2] = __builtin_fma(code_value_d<MK, 2>(rc), rq, z[2]);
+              z[3] = __builtin_fma(code_value_d<MK, 3>(rc), rq, z[3]);
             }
             *reinterpret_cast<uint32_t*>(smem + addr) = pack_codes_d<MK>(z[0], z[1], z[2], z[3], hi);
           }

@@ -103,9 +103,8 @@ __device__ __forceinline__ float med3(float x, float lo, float hi) {
   return __builtin_amdgcn_fmed3f(x, lo, hi);
 }
 
-// Codes of four requantised values already clamped to [0, hi] (hi <= qmax).
-// Both hardware conversions round to nearest even (int8: float -> u8 with the
-// default rounding mode; the values are non-negative and at most 127).
+// Code word of four values already on the code grid and in range (the
+// hardware conversions then only re-encode them).
 template <int MK>
 __device__ __forceinline__ uint32_t pack_codes(float z0, float z1, float z2, float z3) {
   if constexpr (MK == MK_I8) {
@@ -121,28 +120,38 @@ __device__ __forceinline__ uint32_t pack_codes(float z0, float z1, float z2, flo
 }
 // Requantisation in float64.  The next tensor's code is sat(rne(act(y) / a_out));
 // the epilogues compute z = y / a_out from the exact accumulator with float64
-// constants, clamp it to [0, hi] (hi = min(qmax, cap / a_out)) and round it here
-// to the code grid: int8 to the nearest integer, fp8 to the nearest e4m3fn value
-// (ties to even in both).  float64 carries 53 bits, so a rounding decision can
-// differ from exact arithmetic only within about 2^-45 of a tie.
-template <int MK>
-__device__ __forceinline__ float code_round(double z) {
-  if constexpr (MK == MK_I8) {
-    return (float)__builtin_rint(z);
-  } else {
-    // spacing of e4m3 values around z: 2^(e-3) with e = floor(log2 z), at least
-    // -6 (subnormals share the spacing 2^-9); z <= 448 never rounds past 448
-    const int e = max(__builtin_amdgcn_frexp_exp(z) - 1, -6);
-    return (float)__builtin_amdgcn_ldexp(__builtin_rint(__builtin_amdgcn_ldexp(z, 3 - e)), e - 3);
-  }
+// constants and round it here to the code grid (int8: the nearest integer; fp8:
+// the nearest e4m3fn value; ties to even in both), then clamp the code to
+// [0, hi], hi the tensor's largest code (rne(min(qmax, cap / a_out)) on the
+// grid).  Rounding to the grid is monotone, so clamping the rounded value is
+// rounding the clamped one.  float64 carries 53 bits, so a code can differ from
+// exact arithmetic only within about 2^-45 of a tie.
+//
+// int8: adding 1.5 * 2^52 to z (|z| < 2^31) rounds it to an integer, to
+// nearest even in the default rounding mode, and leaves that integer in the low
+// 32 bits of the sum.
+__device__ __forceinline__ int rne_i32(double z) {
+  return (int)(uint32_t)__builtin_bit_cast(uint64_t, z + 6755399441055744.0);
+}
+// fp8: the spacing of e4m3 values around z is 2^(e-3), e = floor(log2 |z|) but at
+// least -6 (subnormals share the spacing 2^-9)
+__device__ __forceinline__ float e4m3_round_d(double z) {
+  const int e = max(__builtin_amdgcn_frexp_exp(z) - 1, -6);
+  return (float)__builtin_amdgcn_ldexp(__builtin_rint(__builtin_amdgcn_ldexp(z, 3 - e)), e - 3);
 }
 __device__ __forceinline__ double clamp_d(double z, double hi) { return __builtin_fmin(__builtin_fmax(z, 0.0), hi); }
-// Codes of four clamped float64 values (exactly representable after code_round,
-// so the hardware conversions below only re-encode them).
+// Code word of four requantised values.
 template <int MK>
-__device__ __forceinline__ uint32_t pack_codes_d(double z0, double z1, double z2, double z3, double hi) {
-  return pack_codes<MK>(code_round<MK>(clamp_d(z0, hi)), code_round<MK>(clamp_d(z1, hi)),
-                        code_round<MK>(clamp_d(z2, hi)), code_round<MK>(clamp_d(z3, hi)));
+__device__ __forceinline__ uint32_t pack_codes_d(double z0, double z1, double z2, double z3, float hi) {
+  if constexpr (MK == MK_I8) {
+    const int h = (int)hi;
+    const uint32_t c0 = min(max(rne_i32(z0), 0), h), c1 = min(max(rne_i32(z1), 0), h);
+    const uint32_t c2 = min(max(rne_i32(z2), 0), h), c3 = min(max(rne_i32(z3), 0), h);
+    return c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
+  } else {
+    return pack_codes<MK>(med3(e4m3_round_d(z0), 0.0f, hi), med3(e4m3_round_d(z1), 0.0f, hi),
+                          med3(e4m3_round_d(z2), 0.0f, hi), med3(e4m3_round_d(z3), 0.0f, hi));
+  }
 }
 
 // Value of byte R of a code word (codes of post-activation tensors are >= 0
@@ -151,6 +160,11 @@ template <int MK, int R>
 __device__ __forceinline__ float code_value(uint32_t x) {
   if constexpr (MK == MK_I8) return (float)((x >> (8 * R)) & 0xffu);  // codes are 0..127
   else return __builtin_amdgcn_cvt_f32_fp8((int)x, R);
+}
+template <int MK, int R>
+__device__ __forceinline__ double code_value_d(uint32_t x) {
+  if constexpr (MK == MK_I8) return (double)((x >> (8 * R)) & 0xffu);
+  else return (double)__builtin_amdgcn_cvt_f32_fp8((int)x, R);
 }
 
 __device__ __forceinline__ float wave_max(float v) {

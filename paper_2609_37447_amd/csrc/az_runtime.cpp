@@ -236,6 +236,13 @@ uint8_t quant_e4m3(double v) {
   return sign | (uint8_t)(((e + 7) << 3) | mant);
 }
 
+// Value of an e4m3fn code (finite codes only).
+float e4m3_value(uint8_t c) {
+  const int e = (c >> 3) & 15, m = c & 7;
+  const double v = e == 0 ? ldexp((double)m, -9) : ldexp(1.0 + m / 8.0, e - 7);
+  return (float)((c & 0x80) ? -v : v);
+}
+
 enum Kind { K_BF16 = 0, K_I8 = 1, K_F8 = 2 };
 
 // Packs a 3x3 conv W[F][Cin][3][3] (padded to Cp input channels) into A fragments.
@@ -483,8 +490,8 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   const BlobView v = view(s, weights);
   const int g = s.pool_every > 0 ? F / 4 : 0, Fr = F - g, V = s.value_channels, D = s.token_dim;
   std::vector<uint8_t> stem, tower, head, emb, qw, kw, pw;
-  std::vector<float> bias, head_b, fc2w, head_sc, head_bc, fc1t;
-  std::vector<double> qmul, qbias, qres, qhi, pool_m, pool_b, pool_cinv;
+  std::vector<float> bias, qhi, head_b, fc2w, head_sc, head_bc, fc1t;
+  std::vector<double> qmul, qbias, qres, pool_m, pool_b, pool_cinv;
   std::vector<float> emb_sc, emb_bc, wfc1t;
   std::vector<float> pool_wt;
   std::vector<uint32_t> actions;
@@ -571,8 +578,10 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
           }
         for (int k = 0; k < K; ++k) {
           if (k >= 2 && k % 2 == 0) qres[k] = a[k - 2] / a[k];
-          const double c = s.act_cap > 0.0f ? (double)s.act_cap / a[k] : qmax;
-          qhi[k] = c < qmax ? c : qmax;
+          // the largest code: min(qmax, cap / a[k]) rounded to the grid
+          double c = s.act_cap > 0.0f ? (double)s.act_cap / a[k] : qmax;
+          if (c > qmax) c = qmax;
+          qhi[k] = dtype == AZ_INT8 ? (float)quant_i8(c) : e4m3_value(quant_e4m3(c));
         }
       }
       if (dep) {
@@ -638,7 +647,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   std::vector<Sec> secs = {
       {stem.data(), stem.size(), 0}, {tower.data(), tower.size(), 0}, {head.data(), head.size(), 0},
       {bias.data(), bias.size() * 4, 0}, {qmul.data(), qmul.size() * 8, 0},
-      {qres.data(), qres.size() * 8, 0}, {qhi.data(), qhi.size() * 8, 0},
+      {qres.data(), qres.size() * 8, 0}, {qhi.data(), qhi.size() * 4, 0},
       {head_b.data(), head_b.size() * 4, 0}, {dep ? nullptr : v.fc1_w, dep ? 0 : VH * 4, 0},
       {v.fc1_b, (size_t)H * 4, 0}, {dep ? (const void*)v.fc2_w : fc2w.data(), (dep ? 3 : 1) * (size_t)H * 4, 0},
       {head_sc.data(), head_sc.size() * 4, 0}, {head_bc.data(), head_bc.size() * 4, 0},
@@ -695,7 +704,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   d.bias = atf(3);
   d.qmul = atd(4);
   d.qres = atd(5);
-  d.qhi = atd(6);
+  d.qhi = atf(6);
   d.qbias = atd(28);
   d.head_b = atf(7);
   d.fc1_w = atf(8);
