@@ -40,23 +40,46 @@ def is_deployed(shape):
     return getattr(shape, "policy_head", "planes") == "fromto"
 
 
-def kernel_source(shape):
-    return os.path.join(CSRC, "az_dep_kernel.h" if is_deployed(shape) else "az_kernels_mfma.hip")
+def kernel_sources(shape, dtype):
+    """The source files the kernel of a workload is compiled from."""
+    if dtype == "f32":
+        main = "az_kernels_f32.hip"
+    else:
+        main = "az_dep_kernel.h" if is_deployed(shape) else "az_kernels_mfma.hip"
+    return [os.path.join(CSRC, f) for f in (main, "az_mfma_common.h", "az_internal.h")]
 
-# HBM traffic of the fused kernel from rocprofv3 --pmc passes (FETCH_SIZE, then
-# WRITE_SIZE, KiB per dispatch), scaled by what the same counters read for a plain
-# copy kernel of known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  An entry holds
-# for the kernel source it was taken on only: any other source reports null.
+
+def kernel_sha(shape, dtype):
+    """sha256 over the kernel's source files, in order."""
+    h = hashlib.sha256()
+    for f in kernel_sources(shape, dtype):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+# Counters of the fused kernel from rocprofv3 --pmc passes (profiles/ holds each
+# summary with its commands): HBM traffic as FETCH_SIZE and WRITE_SIZE (KiB per
+# dispatch), scaled by what the same counters read for a plain copy kernel of
+# known size (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0), and the MFMA busy fraction
+# SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE per XCD x 1024 SIMDs).  An entry
+# holds for the kernel sources it was taken on only (kernel_sha): any other
+# source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
-TRAFFIC = {  # (workload, tiling, batch): (sha256 of the kernel source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    ("net20x128_int8_b1024", 3, 1024): ("717d988db19f736efa011393b8e7c47101967530587d5b80e61dadfe552894a9",
-                                        33295.9, 18704.0),
-    ("net20x128_int8_b1024", 2, 64): ("717d988db19f736efa011393b8e7c47101967530587d5b80e61dadfe552894a9",
-                                      24476.5, 1682.0),
-    ("deployed14x160_int8_b1024", 1, 1024): ("0dbc1335fc2eee0c035cb2fd72b845e67340d305a331eca66c22c0af0e2148ee",
-                                             46252.7, 30174.7),
-    ("deployed14x160_int8_b1024", 2, 64): ("0dbc1335fc2eee0c035cb2fd72b845e67340d305a331eca66c22c0af0e2148ee",
-                                           29524.5, 472.0),
+# (workload, tiling, batch): (kernel_sha, FETCH_SIZE KiB, WRITE_SIZE KiB, MFMA busy fraction)
+COUNTERS = {
+    ("net20x128_bf16_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 52014.8, 18696.0, 0.6446),
+    ("net20x128_bf16_b256", 2, 256): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 48117.8, 4680.0, 0.5002),
+    ("net20x128_fp8_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 29325.3, 18696.0, 0.4462),
+    ("net20x128_int8_b1024", 3, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 36434.1, 18704.0, 0.5764),
+    ("net20x128_int8_b1024", 2, 64): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 24519.3, 1426.0, 0.0861),
+    ("net24x256_bf16_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 453073.7, 27919.5, 0.7451),
+    ("deployed14x160_bf16_b1024", 2, 1024): ("e83ffe3b017010d18cc1a3ee7f5010fb46a158c214407dedbc80065a8eac16df", 222207.8, 7552.0, 0.4080),
+    ("deployed14x160_int8_b1024", 1, 1024): ("e83ffe3b017010d18cc1a3ee7f5010fb46a158c214407dedbc80065a8eac16df", 36525.0, 7552.0, 0.4879),
+    ("deployed14x160_int8_b1024", 2, 64): ("e83ffe3b017010d18cc1a3ee7f5010fb46a158c214407dedbc80065a8eac16df", 29628.3, 472.0, 0.0712),
+    ("net20x128_bf16_b32", 2, 32): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 47039.8, 585.0, 0.0643),
+    ("net20x128_int8_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 29252.8, 18696.0, 0.5106),
+    ("tiny_2x32_f32_b16", 0, 16): ("1566be512ee6b8772c3912e6aff082d6d397e991e8c3d15c06888399d186737a", 1011.0, 292.5, 0.0000),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
@@ -104,15 +127,13 @@ def roofline_peak(shape, dtype):
     return sum(flop.values()), sum(flop.values()) / t_floor
 
 
-def traffic_bytes(w, tiling, B):
-    """Scaled HBM bytes per launch, or None without counters for this exact kernel."""
-    e = TRAFFIC.get((w.name, tiling, B))
-    if e is None:
-        return None
-    with open(kernel_source(w.shape), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != e[0]:
-            return None
-    return (e[1] * FETCH_SCALE + e[2] * WRITE_SCALE) * 1024.0
+def counters_for(w, tiling, B):
+    """(scaled HBM bytes per launch, MFMA busy fraction), or (None, None) without
+    counters taken on this exact kernel source."""
+    e = COUNTERS.get((w.name, tiling, B))
+    if e is None or kernel_sha(w.shape, w.dtype) != e[0]:
+        return None, None
+    return (e[1] * FETCH_SCALE + e[2] * WRITE_SCALE) * 1024.0, e[3]
 
 
 def load_scales(w):
@@ -360,6 +381,7 @@ def main():
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)
     achieved = flop_pos * B / (ms * 1e-3)
+    traffic, mfma_busy = counters_for(w, tiling, B)
     out = {
         "metric": "positions evaluated/sec (policy+value), one az_eval_batch per step",
         "value": B / (ms * 1e-3),
@@ -381,7 +403,8 @@ def main():
                    "params": w.shape.weight_count(), "flop_per_position": flop_pos},
         "roofline": {"bound": "mfma" if w.dtype != "f32" else "alu", "achieved": achieved / 1e12,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_bytes(w, tiling, B), "traffic_unit": "bytes per launch"},
+                     "traffic": traffic, "traffic_unit": "bytes per launch",
+                     "mfma_busy": mfma_busy},
         "latency_us": {"p10": float(np.percentile(lat, 10)), "p50": float(np.percentile(lat, 50)),
                        "p90": float(np.percentile(lat, 90)), "calls": int(lat.size)},
         "graph_replay_us": graph_us,
