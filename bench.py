@@ -9,6 +9,9 @@ batch 1024.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--tiling 0|1|2|3]
 
+Before the W warm-up steps, untimed calls run for 0.3 s so that the timed
+region sees the GPU at its working clock rather than its ramp from idle.
+
 Prints one JSON line on stdout.  --gpus N with N > 1 exits with a message: this
 library evaluates on one GPU (positions are independent; a multi-GPU server
 would run one handle per GPU on its share of the batch).
@@ -193,79 +196,50 @@ def cpu_model():
     return None
 
 
-def pipeline_rates(az, net, w, planes, legal, batches=100, warm=10, max_legal=256):
-    """Positions/s through az_pipeline, host buffers to host buffers: inputs
-    copied from pinned memory, evaluation, outputs back in host memory.  Worker
-    threads share one pipeline; each owns some of its slots and keeps them in
-    flight round-robin (wait for the slot, resubmit it).  Three set-ups: dense
-    policy, one worker with four slots of the full batch; the same with the
-    compact legal-move policy; and four workers with two outstanding batches of
-    320 each, compact.  Each worker runs `warm` batches untimed, then `batches`
-    timed ones.  Measured after the timed region; never the headline value."""
-    import threading
+PIPELINE_LEGS = ("dense_1w4s", "compact_1w4s", "compact_4w2s_b320", "compact_4w2s_b320_graphs")
+SETTLE_S = 0.3
 
+
+def pipeline_rates(az, net, w, planes, legal, batches=100, warm=10, max_legal=256, legs=PIPELINE_LEGS):
+    """Positions/s through az_pipeline, host buffers to host buffers: inputs
+    copied from pinned memory, evaluation, outputs back in host memory.  The
+    library's own worker threads (az_pipeline_drive) share one pipeline; each
+    owns some of its slots and keeps them in flight round-robin (wait for the
+    slot, resubmit it).  Three set-ups: dense policy, one worker with four slots
+    of the full batch; the same with the compact legal-move policy; and four
+    workers with two outstanding batches of 320 each, compact (the paper's
+    retained actor topology, Section 5.2), once on the pipeline's three shared
+    streams and once with each slot replaying its own captured graph.  Each
+    worker runs `warm` batches untimed, then `batches` timed ones.  Measured
+    after the timed region; never the headline value."""
     B = w.batch
     n_moves = w.shape.n_moves
-    res = {"max_legal": max_legal,
+    res = {"max_legal": max_legal, "driver": "az_pipeline_drive (native worker threads)",
            "bytes_in_per_position": int(planes[0].nbytes + legal[0].nbytes),
            "bytes_out_per_position_dense": int((n_moves + 1) * 4),
            "bytes_out_per_position_compact": int((max_legal + 2) * 4)}
-    n = batches
     has = legal.any(axis=1)
-    for name, workers, per_worker, batch, K in (("dense_1w4s_b%d" % B, 1, 4, B, 0),
-                                                ("compact_1w4s_b%d" % B, 1, 4, B, max_legal),
-                                                ("compact_4w2s_b320", 4, 2, min(320, B), max_legal)):
+    setups = (("dense_1w4s", 1, 4, B, 0, False), ("compact_1w4s", 1, 4, B, max_legal, False),
+              ("compact_4w2s_b320", 4, 2, min(320, B), max_legal, False),
+              ("compact_4w2s_b320_graphs", 4, 2, min(320, B), max_legal, True))
+    for leg, workers, per_worker, batch, K, graphs in setups:
+        if leg not in legs:
+            continue
+        name = leg if "b320" in leg else "%s_b%d" % (leg, B)
         slots = workers * per_worker
         spec = az.spec_from_shape(w.shape, batch)
-        pipe = az.Pipeline(net, spec, batch, slots, False, max_legal=K)
+        pipe = az.Pipeline(net, spec, batch, slots, graphs, max_legal=K)
         try:
             for k in range(slots):
                 pipe.views[k][0][:] = planes[:batch]
                 pipe.views[k][1][:] = legal[:batch]
-                pipe.submit(k, batch)
-            for k in range(slots):
-                pipe.wait(k)
-            go = threading.Barrier(workers + 1)
-            timed = threading.Barrier(workers + 1)
-            errors = []
-
-            def run(mine):
-                go.wait()
-                try:
-                    for phase, count in (("warm", warm), ("timed", n)):
-                        if phase == "timed":
-                            timed.wait()
-                        for i in range(count):
-                            k = mine[i % len(mine)]
-                            pipe.wait(k)
-                            pipe.submit(k, batch)
-                        for k in mine:
-                            pipe.wait(k)
-                except Exception as e:  # reported below
-                    errors.append(e)
-                    timed.abort()
-
-            th = [threading.Thread(target=run, args=(list(range(j * per_worker, (j + 1) * per_worker)),))
-                  for j in range(workers)]
-            for t in th:
-                t.start()
-            go.wait()
-            try:
-                timed.wait()
-            except threading.BrokenBarrierError:
-                pass
-            t0 = time.perf_counter()
-            for t in th:
-                t.join()
-            dt = time.perf_counter() - t0
-            if errors:
-                raise errors[0]
+            dt = pipe.drive(workers, per_worker, batch, warm, batches)
             # every legal move fits in max_legal here, so compact rows sum to one too
             v = pipe.views[slots - 1]
             assert np.all(np.abs(v[2][:batch][has[:batch]].sum(axis=1) - 1.0) < 1e-3), "pipeline outputs invalid"
         finally:
             pipe.close()
-        res[name] = {"positions_per_s": workers * n * batch / dt, "batches": workers * n,
+        res[name] = {"positions_per_s": workers * batches * batch / dt, "batches": workers * batches,
                      "warmup_batches": workers * warm}
     return res
 
@@ -287,6 +261,8 @@ def main():
                     help="skip the host-buffer (PCIe-inclusive) pipeline measurement")
     ap.add_argument("--pipeline-batches", type=int, default=100,
                     help="timed batches per worker in each pipeline set-up (after 10 untimed)")
+    ap.add_argument("--pipeline-legs", default=",".join(PIPELINE_LEGS),
+                    help="comma-separated pipeline set-ups to measure: " + ", ".join(PIPELINE_LEGS))
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -323,6 +299,20 @@ def main():
     def step():
         step_on(sp)
 
+    # Before the warm-up steps: untimed calls for at least SETTLE_S seconds.  An
+    # idle GPU needs tens of milliseconds of load to reach its working clock, so
+    # a short timed region right after a few warm-up steps measures that ramp
+    # (20 steps after 5 warm-up ones timed 398 us per batch where 200 after 20
+    # timed 334 us on the same box).
+    t_settle = time.perf_counter()
+    n_settle = 0
+    while True:
+        for _ in range(8):
+            step()
+        n_settle += 8
+        torch.cuda.synchronize()
+        if time.perf_counter() - t_settle >= SETTLE_S:
+            break
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -375,8 +365,8 @@ def main():
         torch.cuda.synchronize()
         graph_us = g0.elapsed_time(g1) * 1000.0 / n_rep
         del g
-    pipeline = None if (args.no_pipeline or B != w.batch) else pipeline_rates(az, net, w, planes, legal,
-                                                                               args.pipeline_batches)
+    pipeline = None if (args.no_pipeline or B != w.batch) else pipeline_rates(
+        az, net, w, planes, legal, args.pipeline_batches, legs=tuple(args.pipeline_legs.split(",")))
     az.az_net_free(net)
 
     flop_pos, peak = roofline_peak(w.shape, w.dtype)
@@ -411,6 +401,7 @@ def main():
         "pipeline_pcie_inclusive": pipeline,
         "outputs_valid": ok,
         "wall_s_timed": wall,
+        "settle": {"seconds": SETTLE_S, "calls": n_settle},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, blob, ws, acs, planes, legal, args.cpu_budget)

@@ -339,6 +339,20 @@ int az_pipeline_query(az_pipeline* p, int32_t slot);
  * az_pipeline_query apart from 1. */
 int az_pipeline_wait(az_pipeline* p, int32_t slot);
 
+/* Drives the pipeline from `workers` native threads, the actors of the paper's
+ * host side (Section 5.1 "Native ownership of the search loop", Section 5.2
+ * "Batching and host-side submission"): worker w owns slots w*slots_per_worker
+ * .. (w+1)*slots_per_worker - 1 and keeps them in flight round-robin (wait for
+ * the slot, resubmit its current host inputs as a batch of B positions), first
+ * `warmup` submissions untimed, then `batches` timed ones, each phase ending
+ * with all of the worker's slots drained.  *seconds receives the wall time of
+ * the timed phase (from the moment every worker has drained its warm-up).  The
+ * caller fills the slots' inputs beforehand and must not use the pipeline
+ * meanwhile.  Returns AZ_OK or the first failing status (AZ_ERR_INVALID_ARG for
+ * bad counts, including a compact row that overflowed max_legal). */
+int az_pipeline_drive(az_pipeline* p, int32_t workers, int32_t slots_per_worker, int32_t B, int32_t warmup,
+                      int32_t batches, double* seconds);
+
 /* Waits for every slot, then frees the pipeline's buffers, streams, events and
  * graphs; NULL is a no-op. */
 void az_pipeline_free(az_pipeline* p);

@@ -14,4 +14,4 @@ from ._binding import (AZ_ABI_VERSION, AZ_BF16, AZ_ERR_DEVICE, AZ_ERR_INVALID_AR
                        make_spec, spec_from_shape, validate, Pipeline, AZ_PIPE_COMPACT_POLICY, AZ_PIPE_GRAPHS,
                        az_pipeline_create,
                        az_pipeline_free, az_pipeline_query, az_pipeline_slot, az_pipeline_submit,
-                       az_pipeline_wait, az_debug_fail_allocation, az_debug_live_allocations)
+                       az_pipeline_wait, az_pipeline_drive, az_debug_fail_allocation, az_debug_live_allocations)

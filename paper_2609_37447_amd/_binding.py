@@ -27,7 +27,8 @@ EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_eval_batch_wdl
            "az_net_set_tiling",
            "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_compare_outputs",
            "az_pipeline_create", "az_pipeline_slot", "az_pipeline_submit", "az_pipeline_query",
-           "az_pipeline_wait", "az_pipeline_free", "az_debug_fail_allocation", "az_debug_live_allocations",
+           "az_pipeline_wait", "az_pipeline_drive", "az_pipeline_free", "az_debug_fail_allocation",
+           "az_debug_live_allocations",
            "az_status_string", "az_last_error")
 
 
@@ -64,6 +65,11 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with "
                               "`python -m paper_2609_37447_amd.build`")
+        # torch ships its own HIP runtime under the same soname as ROCm's
+        # (libamdhip64.so.7).  Loading torch first makes this library bind to
+        # that one copy; loaded the other way round, torch would bring up a
+        # second runtime beside it and find no GPU.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
         FP = ctypes.POINTER(ctypes.c_float)
@@ -91,6 +97,8 @@ def lib():
         L.az_pipeline_query.argtypes, L.az_pipeline_query.restype = [P, I32], ctypes.c_int
         L.az_pipeline_wait.argtypes, L.az_pipeline_wait.restype = [P, I32], ctypes.c_int
         L.az_pipeline_free.argtypes, L.az_pipeline_free.restype = [P], None
+        L.az_pipeline_drive.argtypes = [P, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_double)]
+        L.az_pipeline_drive.restype = ctypes.c_int
         L.az_debug_fail_allocation.argtypes, L.az_debug_fail_allocation.restype = [I32], None
         L.az_debug_live_allocations.argtypes, L.az_debug_live_allocations.restype = [], ctypes.c_int64
         L.az_status_string.argtypes, L.az_status_string.restype = [ctypes.c_int], ctypes.c_char_p
@@ -310,6 +318,14 @@ def az_pipeline_wait(p, slot: int) -> int:
     return _check(lib().az_pipeline_wait(p, slot), "az_pipeline_wait")
 
 
+def az_pipeline_drive(p, workers: int, slots_per_worker: int, B: int, warmup: int, batches: int) -> float:
+    """Wall seconds of `batches` native round-robin submissions per worker thread."""
+    sec = ctypes.c_double()
+    _check(lib().az_pipeline_drive(p, workers, slots_per_worker, B, warmup, batches, ctypes.byref(sec)),
+           "az_pipeline_drive")
+    return sec.value
+
+
 def az_pipeline_free(p) -> None:
     lib().az_pipeline_free(p)
 
@@ -345,6 +361,9 @@ class Pipeline:
 
     def query(self, slot: int) -> bool:
         return az_pipeline_query(self.p, slot) == 0
+
+    def drive(self, workers: int, slots_per_worker: int, B: int, warmup: int, batches: int) -> float:
+        return az_pipeline_drive(self.p, workers, slots_per_worker, B, warmup, batches)
 
     def close(self) -> None:
         if self.p is not None:

@@ -30,8 +30,12 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <chrono>
+#include <condition_variable>
 #include <mutex>
 #include <new>
+#include <string>
+#include <thread>
 #include <vector>
 
 #include "az.h"
@@ -422,6 +426,75 @@ int az_pipeline_wait(az_pipeline* p, int32_t slot) {
   if (e != hipSuccess) return hip_err(e, "az_pipeline_wait");
   s.submitted = false;
   return check_counts(p, s);
+}
+
+int az_pipeline_drive(az_pipeline* p, int32_t workers, int32_t slots_per_worker, int32_t B, int32_t warmup,
+                      int32_t batches, double* seconds) {
+  if (!p || !seconds) return az_fail(AZ_ERR_INVALID_ARG, "az_pipeline_drive: NULL argument");
+  if (workers < 1 || slots_per_worker < 1 || (int64_t)workers * slots_per_worker > (int64_t)p->slots.size())
+    return az_fail(AZ_ERR_INVALID_ARG, "az_pipeline_drive: workers x slots_per_worker exceeds the pipeline's slots");
+  if (B < 1 || B > p->max_batch) return az_fail(AZ_ERR_INVALID_ARG, "az_pipeline_drive: B out of range");
+  if (warmup < 0 || batches < 1) return az_fail(AZ_ERR_INVALID_ARG, "az_pipeline_drive: bad batch counts");
+  // A barrier between the warm-up and the timed part: the main thread starts
+  // the clock once every worker has drained its warm-up submissions.
+  // Error messages are per thread: a worker's is copied out and set again on
+  // the calling thread.
+  std::mutex mu;
+  std::condition_variable cv;
+  int arrived = 0;
+  bool go = false, abandon = false;
+  std::vector<int> status(workers, AZ_OK);
+  std::vector<std::string> message(workers);
+  auto run = [&](int w) {
+    const int s0 = w * slots_per_worker;
+    auto phase = [&](int count) {
+      for (int i = 0; i < count; ++i) {
+        const int k = s0 + i % slots_per_worker;
+        int st = az_pipeline_wait(p, k);
+        if (st == AZ_OK) st = az_pipeline_submit(p, k, B);
+        if (st != AZ_OK) return st;
+      }
+      for (int k = s0; k < s0 + slots_per_worker; ++k) {
+        const int st = az_pipeline_wait(p, k);
+        if (st != AZ_OK) return st;
+      }
+      return (int)AZ_OK;
+    };
+    int st = phase(warmup);
+    {
+      std::unique_lock<std::mutex> lock(mu);
+      ++arrived;
+      cv.notify_all();
+      cv.wait(lock, [&] { return go; });
+    }
+    if (st == AZ_OK && !abandon) st = phase(batches);
+    status[w] = st;
+    if (st != AZ_OK) message[w] = az_last_error();
+  };
+  std::vector<std::thread> th;
+  try {
+    for (int w = 0; w < workers; ++w) th.emplace_back(run, w);
+  } catch (...) {
+    {
+      std::lock_guard<std::mutex> lock(mu);
+      go = abandon = true;
+    }
+    cv.notify_all();
+    for (auto& t : th) t.join();
+    return az_fail(AZ_ERR_NOMEM, "az_pipeline_drive: could not start the worker threads");
+  }
+  {
+    std::unique_lock<std::mutex> lock(mu);
+    cv.wait(lock, [&] { return arrived == workers; });
+    go = true;
+  }
+  const auto t0 = std::chrono::steady_clock::now();
+  cv.notify_all();
+  for (auto& t : th) t.join();
+  *seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  for (int w = 0; w < workers; ++w)
+    if (status[w] != AZ_OK) return az_fail(status[w], message[w].c_str());
+  return AZ_OK;
 }
 
 void az_pipeline_free(az_pipeline* p) {

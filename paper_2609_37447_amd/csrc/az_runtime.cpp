@@ -376,10 +376,11 @@ int choose_tiling(const az_net* n, int B) {
   if (is_deployed(n->spec)) return choose_dep_tiling(n, B);
   const int F = n->spec.filters;
   if (B < 512) return 2;
-  // int8's one-board tiling, with its 18-step weight ring, runs 768 boards in
-  // 268 us against 280 for the medium tiling, 1,024 in 344 against 318
-  if (n->dtype == AZ_INT8 && B <= 768) return 2;
-  if (n->dtype == AZ_BF16) return B >= 1024 ? 1 : 2;
+  // Measured on 20x128 (us per batch, large / one-board / medium tiling):
+  // int8 768 boards 293 / 283 / 295, 896 boards 303 / 342 / 311, 1,024 boards
+  // 327 / 368 / 338; bf16 640 boards 487 / 459 / 458, 768 boards 495 / 510 / 512.
+  if (n->dtype == AZ_INT8) return B <= 768 ? 2 : 1;
+  if (n->dtype == AZ_BF16) return B >= 768 ? 1 : 2;
   if (n->dtype == AZ_FP8_E4M3 && B >= 1024) return 1;
   return az_mfma_tiling_valid(F, 3) ? 3 : 1;
 }

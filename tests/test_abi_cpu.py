@@ -189,4 +189,7 @@ def test_pipeline_rejects_bad_arguments_before_device():
         assert fn(None, 0) == az.AZ_ERR_INVALID_ARG
     assert L.az_pipeline_submit(None, 0, 1) == az.AZ_ERR_INVALID_ARG
     assert L.az_pipeline_slot(None, 0, None, None, None, None, None) == az.AZ_ERR_INVALID_ARG
+    sec = ctypes.c_double()
+    assert L.az_pipeline_drive(None, 1, 1, 1, 0, 1, ctypes.byref(sec)) == az.AZ_ERR_INVALID_ARG
+    assert b"az_pipeline_drive" in L.az_last_error()
     L.az_pipeline_free(None)                                 # no-op

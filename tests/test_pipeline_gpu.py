@@ -2,6 +2,8 @@
 az_eval_batch on the same inputs, bit for bit, with and without graph replay,
 over several slots in flight at once and changing batch sizes (needs gfx950)."""
 
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -230,6 +232,61 @@ def test_pipeline_worker_threads_share_one_pipeline():
             t.join()
         if errors:
             raise errors[0]
+    finally:
+        if pipe is not None:
+            pipe.close()
+        az.az_net_free(net)
+
+
+@pytest.mark.parametrize("use_graphs", [False, True])
+def test_native_driver_outputs_and_statuses(use_graphs):
+    # az_pipeline_drive resubmits each slot's resident inputs from native worker
+    # threads; afterwards every slot holds the compact outputs of its own inputs
+    import torch
+
+    import paper_2609_37447_amd as az
+    w = W["net20x128_int8_b1024"]
+    blob = azgen.workload_weights(w)
+    ws, acs = H.quant_scales(w.name, "int8")
+    MB, K, WORKERS, PER = 64, 64, 3, 2
+    _print(f"case native driver int8 graphs={use_graphs} workers={WORKERS}x{PER} max_batch={MB}")
+    spec = az.spec_from_shape(w.shape, MB)
+    net = az.az_net_load(spec, blob, "int8", ws, acs)
+    pipe = None
+    try:
+        pipe = az.Pipeline(net, spec, MB, WORKERS * PER, use_graphs, max_legal=K)
+        dev = torch.device("cuda:0")
+        want = []
+        for k in range(WORKERS * PER):
+            planes, legal = azgen.make_inputs(w, n=MB, seed=900 + k)
+            pipe.views[k][0][:] = planes
+            pipe.views[k][1][:] = legal
+            P0 = torch.empty((MB, w.shape.n_moves), device=dev)
+            V0 = torch.empty((MB,), device=dev)
+            az.eval_tensors(net, torch.from_numpy(planes).to(dev), torch.from_numpy(legal).to(dev), P0, V0)
+            want.append(_compact_definition(P0.cpu().numpy(), legal, K) + (V0.cpu().numpy(),))
+        torch.cuda.synchronize()
+        sec = pipe.drive(WORKERS, PER, MB, 4, 8)
+        assert sec > 0.0
+        for k in range(WORKERS * PER):
+            _, _, po, va, cnt = pipe.views[k]
+            wp, wc, wv = want[k]
+            assert np.array_equal(cnt, wc), f"slot {k} counts"
+            assert np.array_equal(po, wp), f"slot {k} policy"
+            assert np.array_equal(va, wv), f"slot {k} value"
+        # bad arguments: nothing is submitted
+        L, sec_c = az.lib(), ctypes.c_double()
+        bad = [(0, PER, MB, 0, 1), (WORKERS, PER + 1, MB, 0, 1), (WORKERS, PER, MB + 1, 0, 1),
+               (WORKERS, PER, 0, 0, 1), (WORKERS, PER, MB, -1, 1), (WORKERS, PER, MB, 0, 0)]
+        for a in bad:
+            assert L.az_pipeline_drive(pipe.p, *a, ctypes.byref(sec_c)) == az.AZ_ERR_INVALID_ARG, a
+        assert L.az_pipeline_drive(pipe.p, WORKERS, PER, MB, 0, 1, None) == az.AZ_ERR_INVALID_ARG
+        # a row with more than max_legal legal cells surfaces from a worker thread
+        # with its message on the calling thread
+        pipe.views[1][1][5, :] = 1
+        st = L.az_pipeline_drive(pipe.p, WORKERS, PER, MB, 0, 2, ctypes.byref(sec_c))
+        assert st == az.AZ_ERR_INVALID_ARG, st
+        assert b"max_legal" in L.az_last_error(), L.az_last_error()
     finally:
         if pipe is not None:
             pipe.close()
