@@ -135,6 +135,23 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
   // fp32 residual stream of the wave's output tile (bf16 networks)
   float res[QUANT ? 1 : MBW][QUANT ? 1 : NBW][16];
 
+  // The four-board tilings (one workgroup per CU) have registers to spare
+  // outside the tower: they load the stem's and the heads' weights early.
+  constexpr bool ROOMY = OCC == 1 && NBW >= 4;
+  // Stem weights (bf16, K = 288 in nine taps of two steps): a ring of SR taps,
+  // the first SR - 1 loaded here, ahead of the input planes, so that their
+  // latency overlaps the ingest: all nine taps, or double-buffered.
+  constexpr int SR = ROOMY ? 9 : 2, SSTEP = NMB * 64 * 16;
+  const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)(mb0 * 64 + lane) * 16;
+  SB::frag sa[SR][2][MBW];
+  auto load_stem_tap = [&](int tap, SB::frag(&dst)[2][MBW]) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int m = 0; m < MBW; ++m) dst[s][m] = g_frag<MK_BF16>(sw8 + (tap * 2 + s) * SSTEP + m * 64 * 16);
+  };
+  static_for<0, SR - 1>([&](auto t_c) { load_stem_tap(decltype(t_c)::value, sa[decltype(t_c)::value]); });
+
   // ---- ingest: zero row, planes -> bf16 [board][square][32 channels] at OFF_T
   for (int i = tid; i < C::ZB / 16; i += NT)
     *reinterpret_cast<i32x4*>(smem + OFF_Z + i * 16) = i32x4{0, 0, 0, 0};
@@ -222,14 +239,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
 
   // ---- stem: bf16 3x3 conv over 32 (padded) input channels, K = 288
   {
-    constexpr int SSTEP = NMB * 64 * 16;
-    const uint8_t* sw8 = static_cast<const uint8_t*>(p.stem_w) + (size_t)(mb0 * 64 + lane) * 16;
     f32x16 sacc[MBW][NBW];
-    SB::frag a[2][2][MBW];
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int m = 0; m < MBW; ++m) a[0][s][m] = g_frag<MK_BF16>(sw8 + s * SSTEP + m * 64 * 16);
     int row[NBW], sw[NBW], nrow[NBW], nsw[NBW];
     SB::frag bc[NBW], bn[NBW];
 #pragma unroll
@@ -239,12 +249,8 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     }
 #pragma unroll
     for (int tap = 0; tap < 9; ++tap) {
+      if (tap + SR - 1 < 9) load_stem_tap(tap + SR - 1, sa[(tap + SR - 1) % SR]);
       if (tap + 1 < 9) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int m = 0; m < MBW; ++m)
-            a[(tap + 1) & 1][s][m] = g_frag<MK_BF16>(sw8 + ((tap + 1) * 2 + s) * SSTEP + m * 64 * 16);
 #pragma unroll
         for (int n = 0; n < NBW; ++n) tap_row<64>(tap + 1, OFF_T, OFF_Z, nb0 + n, l32, nrow[n], nsw[n]);
       }
@@ -261,7 +267,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
         for (int m = 0; m < MBW; ++m)
 #pragma unroll
           for (int n = 0; n < NBW; ++n)
-            sacc[m][n] = SB::mma(a[tap & 1][s][m], bc[n], (tap == 0 && s == 0) ? f32x16{} : sacc[m][n]);
+            sacc[m][n] = SB::mma(sa[tap % SR][s][m], bc[n], (tap == 0 && s == 0) ? f32x16{} : sacc[m][n]);
 #pragma unroll
         for (int n = 0; n < NBW; ++n) bc[n] = bn[n];
       }
@@ -544,6 +550,17 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     }
   {
     constexpr int HS = F / 16, RBX = C::RBX, OFF_X = C::OFF_X, NBH = C::NBH;
+    // head weights: in flight during the conversion below where the registers
+    // allow, else loaded after it
+    SB::frag ha[HS][3];
+    auto load_head_w = [&]() {
+      const uint8_t* hw = static_cast<const uint8_t*>(p.head_w) + (size_t)lane * 16;
+#pragma unroll
+      for (int s = 0; s < HS; ++s)
+#pragma unroll
+        for (int m = 0; m < 3; ++m) ha[s][m] = g_frag<MK_BF16>(hw + ((s * 3 + m) * 64) * 16);
+    };
+    if constexpr (ROOMY) load_head_w();
     if constexpr (QUANT) {
       // codes -> exact bf16 values (int8 and e4m3 values are bf16-representable)
       for (int idx = tid; idx < BPW * 64 * (F / 8); idx += NT) {
@@ -574,12 +591,7 @@ az_net_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
           }
         }
     }
-    SB::frag ha[HS][3];
-    const uint8_t* hw = static_cast<const uint8_t*>(p.head_w) + (size_t)lane * 16;
-#pragma unroll
-    for (int s = 0; s < HS; ++s)
-#pragma unroll
-      for (int m = 0; m < 3; ++m) ha[s][m] = g_frag<MK_BF16>(hw + ((s * 3 + m) * 64) * 16);
+    if constexpr (!ROOMY) load_head_w();
     __syncthreads();
 
     f32x16 hacc[NBH][3];

@@ -139,14 +139,21 @@ __device__ __forceinline__ float e4m3_round_d(double z) {
   const int e = max(__builtin_amdgcn_frexp_exp(z) - 1, -6);
   return (float)__builtin_amdgcn_ldexp(__builtin_rint(__builtin_amdgcn_ldexp(z, 3 - e)), e - 3);
 }
+// min(max(x, lo), hi) for lo <= hi in one instruction (the compiler forms it
+// only when it can prove lo <= hi)
+__device__ __forceinline__ int med3_i32(int x, int lo, int hi) {
+  int r;
+  asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(lo), "v"(hi));
+  return r;
+}
 __device__ __forceinline__ double clamp_d(double z, double hi) { return __builtin_fmin(__builtin_fmax(z, 0.0), hi); }
 // Code word of four requantised values.
 template <int MK>
 __device__ __forceinline__ uint32_t pack_codes_d(double z0, double z1, double z2, double z3, float hi) {
   if constexpr (MK == MK_I8) {
-    const int h = (int)hi;
-    const uint32_t c0 = min(max(rne_i32(z0), 0), h), c1 = min(max(rne_i32(z1), 0), h);
-    const uint32_t c2 = min(max(rne_i32(z2), 0), h), c3 = min(max(rne_i32(z3), 0), h);
+    const int h = (int)hi;  // >= 0
+    const uint32_t c0 = med3_i32(rne_i32(z0), 0, h), c1 = med3_i32(rne_i32(z1), 0, h);
+    const uint32_t c2 = med3_i32(rne_i32(z2), 0, h), c3 = med3_i32(rne_i32(z3), 0, h);
     return c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
   } else {
     return pack_codes<MK>(med3(e4m3_round_d(z0), 0.0f, hi), med3(e4m3_round_d(z1), 0.0f, hi),
