@@ -185,9 +185,11 @@ struct DepCfg {
   static constexpr int BUF = 64 * RB;
   static constexpr int OFF_H = 0, OFF_T = BUF, OFF_Z = 2 * BUF;
   static constexpr int ZB = (RB + 256 + 255) / 256 * 256;
-  // per-layer epilogue constants: [bias F] floats, or for int8 [qbias F | qmul F]
-  // doubles (the float64 requantisation)
-  static constexpr int KSLOT = QUANT ? 16 * DF : 4 * DF;
+  // per-layer epilogue constants: [bias F] floats, or for int8 [qbias F | qmul F
+  // | qres, qhi] doubles (the float64 requantisation; the layer's two scalars
+  // ride along so that the epilogue reads them from LDS: a load from global
+  // memory there would wait behind the weight stream)
+  static constexpr int KSLOT = QUANT ? 16 * DF + 16 : 4 * DF;
   static constexpr int OFF_K = OFF_Z + ZB;
   static constexpr int OFF_PG = OFF_K + 2 * KSLOT;    // pooled statistics, 2g doubles
   static constexpr int TOWER_END = OFF_PG + 2 * DG * 8;
@@ -936,7 +938,10 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
     for (int t = 0; t < KPL; ++t) {
       const int i = lane + 64 * t;
       const void* src;
-      if constexpr (QUANT) src = i < DF / 2 ? p.qbias + (size_t)k * DF + 2 * i : p.qmul + (size_t)k * DF + 2 * (i - DF / 2);
+      if constexpr (QUANT)
+        src = i < DF / 2 ? p.qbias + (size_t)k * DF + 2 * i
+              : i < DF   ? p.qmul + (size_t)k * DF + 2 * (i - DF / 2)
+                         : p.qext + 2 * (size_t)k;
       else src = p.bias + (size_t)k * DF + 4 * i;
       dst[t] = i < KV ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
@@ -1246,8 +1251,9 @@ az_dep_kernel(AzDevNet p, const float* __restrict__ planes, const uint8_t* __res
       float hi = 0.0f;
       double rq = 0.0;
       if constexpr (QUANT) {
-        hi = p.qhi[n_conv + 1];
-        rq = SECOND ? p.qres[n_conv + 1] : 0.0;
+        const double* kd = reinterpret_cast<const double*>(kslot);
+        hi = (float)kd[2 * DF + 1];
+        rq = SECOND ? kd[2 * DF] : 0.0;
       }
       constexpr int NRUN = DNMB * 4, EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
       constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place
@@ -1454,7 +1460,10 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
     for (int t = 0; t < KPL; ++t) {
       const int i = tid + NT * t;
       const void* src;
-      if constexpr (QUANT) src = i < DF / 2 ? p.qbias + (size_t)k * DF + 2 * i : p.qmul + (size_t)k * DF + 2 * (i - DF / 2);
+      if constexpr (QUANT)
+        src = i < DF / 2 ? p.qbias + (size_t)k * DF + 2 * i
+              : i < DF   ? p.qmul + (size_t)k * DF + 2 * (i - DF / 2)
+                         : p.qext + 2 * (size_t)k;
       else src = p.bias + (size_t)k * DF + 4 * i;
       dst[t] = i < KV ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
@@ -1789,8 +1798,9 @@ az_dep_kernel4(AzDevNet p, const float* __restrict__ planes, const uint8_t* __re
         float hi = 0.0f;
         double rq = 0.0;
         if constexpr (QUANT) {
-          hi = p.qhi[n_conv + 1];
-          rq = SECOND ? p.qres[n_conv + 1] : 0.0;
+          const double* kd = reinterpret_cast<const double*>(kslot);
+          hi = (float)kd[2 * DF + 1];
+          rq = SECOND ? kd[2 * DF] : 0.0;
         }
         constexpr int EP_AHEAD = 2, EP_RING = EP_AHEAD + 1;
         constexpr bool RCODE = QUANT && SECOND;   // residual codes, read in place

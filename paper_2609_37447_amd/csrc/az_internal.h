@@ -41,6 +41,9 @@ struct AzDevNet {
   // the code grid (activation cap and saturation).
   const double* qres;
   const float* qhi;
+  // qext[2k], qext[2k + 1] = qres[k], qhi[k] (as a double): the two scalars of
+  // tensor k side by side, for kernels that stage them with the per-channel ones
+  const double* qext;
   const float* head_b;  // [AZ_HEAD_ROWS]: policy biases, value conv bias at row P, zeros
   const float* fc1_w;   // [H][64]
   const float* fc1_b;   // [H]

@@ -492,7 +492,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   const int g = s.pool_every > 0 ? F / 4 : 0, Fr = F - g, V = s.value_channels, D = s.token_dim;
   std::vector<uint8_t> stem, tower, head, emb, qw, kw, pw;
   std::vector<float> bias, qhi, head_b, fc2w, head_sc, head_bc, fc1t;
-  std::vector<double> qmul, qbias, qres, pool_m, pool_b, pool_cinv;
+  std::vector<double> qmul, qbias, qres, qext, pool_m, pool_b, pool_cinv;
   std::vector<float> emb_sc, emb_bc, wfc1t;
   std::vector<float> pool_wt;
   std::vector<uint32_t> actions;
@@ -584,6 +584,11 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
           if (c > qmax) c = qmax;
           qhi[k] = dtype == AZ_INT8 ? (float)quant_i8(c) : e4m3_value(quant_e4m3(c));
         }
+        qext.resize((size_t)2 * K);
+        for (int k = 0; k < K; ++k) {
+          qext[2 * k] = qres[k];
+          qext[2 * k + 1] = qhi[k];
+        }
       }
       if (dep) {
         // global pooling (int8): the pooled channels' activation
@@ -660,7 +665,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
       {pool_wt.data(), pool_wt.size() * 4, 0}, {pool_m.data(), pool_m.size() * 8, 0},
       {pool_b.data(), pool_b.size() * 8, 0}, {pool_cinv.data(), pool_cinv.size() * 8, 0},
       {actions.data(), actions.size() * 4, 0}, {wfc1t.data(), wfc1t.size() * 4, 0},
-      {qbias.data(), qbias.size() * 8, 0}};
+      {qbias.data(), qbias.size() * 8, 0}, {qext.data(), qext.size() * 8, 0}};
   size_t total = 0;
   for (auto& sc : secs) { sc.off = total; total += align256(sc.bytes); }
 
@@ -707,6 +712,7 @@ int az_net_load(const az_layer_spec* spec_in, const float* weights, size_t n_wei
   d.qres = atd(5);
   d.qhi = atf(6);
   d.qbias = atd(28);
+  d.qext = atd(29);
   d.head_b = atf(7);
   d.fc1_w = atf(8);
   d.fc1_b = atf(9);
