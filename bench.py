@@ -71,18 +71,18 @@ def kernel_sha(shape, dtype):
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 # (workload, tiling, batch): (kernel_sha, FETCH_SIZE KiB, WRITE_SIZE KiB, MFMA busy fraction)
 COUNTERS = {
-    ("net20x128_bf16_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 52014.8, 18696.0, 0.6446),
-    ("net20x128_bf16_b256", 2, 256): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 48117.8, 4680.0, 0.5002),
-    ("net20x128_fp8_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 29325.3, 18696.0, 0.4462),
-    ("net20x128_int8_b1024", 3, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 36434.1, 18704.0, 0.5764),
-    ("net20x128_int8_b1024", 2, 64): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 24519.3, 1426.0, 0.0861),
-    ("net24x256_bf16_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 453073.7, 27919.5, 0.7451),
-    ("deployed14x160_bf16_b1024", 2, 1024): ("e83ffe3b017010d18cc1a3ee7f5010fb46a158c214407dedbc80065a8eac16df", 222207.8, 7552.0, 0.4080),
-    ("deployed14x160_int8_b1024", 1, 1024): ("e83ffe3b017010d18cc1a3ee7f5010fb46a158c214407dedbc80065a8eac16df", 36525.0, 7552.0, 0.4879),
-    ("deployed14x160_int8_b1024", 2, 64): ("e83ffe3b017010d18cc1a3ee7f5010fb46a158c214407dedbc80065a8eac16df", 29628.3, 472.0, 0.0712),
-    ("net20x128_bf16_b32", 2, 32): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 47039.8, 585.0, 0.0643),
-    ("net20x128_int8_b1024", 1, 1024): ("c89767f5b78e58f9ba13fe814e7ee11923dd175877b7ba713456b8eba2c2e9a5", 29252.8, 18696.0, 0.5106),
-    ("tiny_2x32_f32_b16", 0, 16): ("1566be512ee6b8772c3912e6aff082d6d397e991e8c3d15c06888399d186737a", 1011.0, 292.5, 0.0000),
+    ("net20x128_int8_b1024", 1, 1024): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 29227.8, 18696.0, 0.5248),
+    ("net20x128_int8_b1024", 3, 1024): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 35892.4, 18704.0, 0.5808),
+    ("net20x128_int8_b1024", 2, 64): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 24521.3, 1426.0, 0.1001),
+    ("net20x128_bf16_b1024", 1, 1024): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 51993.8, 18696.0, 0.6404),
+    ("net20x128_bf16_b256", 2, 256): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 48117.3, 4680.0, 0.4941),
+    ("net20x128_bf16_b32", 2, 32): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 47039.3, 585.0, 0.0642),
+    ("net20x128_fp8_b1024", 1, 1024): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 29298.3, 18696.0, 0.4507),
+    ("net24x256_bf16_b1024", 1, 1024): ("7a770b690d9e4ea2135600068b15c968e88a6b3e6bfff5e9e1322192b9faaac5", 449865.3, 18704.6, 0.7573),
+    ("deployed14x160_int8_b1024", 1, 1024): ("5c99920884a7ae6b6f4b20e9d3a337117dccd2719057c9c6ce14ade7bafdd416", 36532.0, 7552.0, 0.4958),
+    ("deployed14x160_int8_b1024", 2, 64): ("5c99920884a7ae6b6f4b20e9d3a337117dccd2719057c9c6ce14ade7bafdd416", 29637.4, 472.0, 0.0743),
+    ("deployed14x160_bf16_b1024", 2, 1024): ("5c99920884a7ae6b6f4b20e9d3a337117dccd2719057c9c6ce14ade7bafdd416", 222194.4, 7552.0, 0.4100),
+    ("tiny_2x32_f32_b16", 0, 16): ("71a6c293790d7c1ed568fe2a55efb4c240b4ffe70594008f8c4af0194bf047ae", 1010.5, 292.5, 0.0000),
 }
 
 # MI355X published dense peaks (FLOP/s) at 2.4 GHz, 256 CUs.
