@@ -357,6 +357,27 @@ int az_pipeline_drive(az_pipeline* p, int32_t workers, int32_t slots_per_worker,
  * graphs; NULL is a no-op. */
 void az_pipeline_free(az_pipeline* p);
 
+/* az_eval_batch followed by the compaction of AZ_PIPE_COMPACT_POLICY, on
+ * device buffers, allocating nothing: for callers that cannot allocate (code
+ * under HIP graph capture, serving loops and harnesses that forbid hipMalloc).
+ * policy: device [B][max_legal] fp32, per position the probabilities of its
+ * legal cells in ascending cell order, zero past the last (a row with more than
+ * max_legal legal cells keeps its first max_legal); legal_count: device [B]
+ * int32, the true number of legal cells; value: device [B] fp32.  planes,
+ * legal as for az_eval_batch.  The dense policy between the two kernels lives
+ * in a static device array of the library, 512 * 95 * 64 floats (12.45 MB)
+ * held by every GPU the library runs on until the process ends: B times
+ * az_net_moves(net) must not exceed it (at most 666 positions of the 4,672-cell
+ * move-plane policy, 1,655 of the 1,880 from-to actions), else
+ * AZ_ERR_INVALID_ARG with a message.  All calls on one GPU share that array:
+ * calls that overlap on one GPU (different streams or threads) race.  B == 0
+ * returns AZ_OK and launches nothing; NULL or misaligned pointers, max_legal
+ * outside 1..az_net_moves(net) and B outside 0..max_batch return
+ * AZ_ERR_INVALID_ARG.  Asynchronous on `stream`, no host synchronisation. */
+int az_eval_batch_compact_noalloc(az_net* net, const float* planes, const uint8_t* legal, int32_t B,
+                                  int32_t max_legal, float* policy, int32_t* legal_count, float* value,
+                                  void* stream);
+
 /* Failure-handling test support.  az_debug_fail_allocation(n), n >= 1: the
  * n-th device or pinned-host allocation the library attempts from now on
  * (weights in az_net_load, buffers in az_pipeline_create) fails as if the

@@ -28,7 +28,7 @@ EXPORTS = ("az_weight_count", "az_net_load", "az_eval_batch", "az_eval_batch_wdl
            "az_net_tiling_for", "az_net_device_bytes", "az_net_free", "az_compare_outputs",
            "az_pipeline_create", "az_pipeline_slot", "az_pipeline_submit", "az_pipeline_query",
            "az_pipeline_wait", "az_pipeline_drive", "az_pipeline_free", "az_debug_fail_allocation",
-           "az_debug_live_allocations",
+           "az_debug_live_allocations", "az_eval_batch_compact_noalloc",
            "az_status_string", "az_last_error")
 
 
@@ -99,6 +99,8 @@ def lib():
         L.az_pipeline_free.argtypes, L.az_pipeline_free.restype = [P], None
         L.az_pipeline_drive.argtypes = [P, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_double)]
         L.az_pipeline_drive.restype = ctypes.c_int
+        L.az_eval_batch_compact_noalloc.argtypes = [P, P, P, I32, I32, P, P, P, P]
+        L.az_eval_batch_compact_noalloc.restype = ctypes.c_int
         L.az_debug_fail_allocation.argtypes, L.az_debug_fail_allocation.restype = [I32], None
         L.az_debug_live_allocations.argtypes, L.az_debug_live_allocations.restype = [], ctypes.c_int64
         L.az_status_string.argtypes, L.az_status_string.restype = [ctypes.c_int], ctypes.c_char_p

@@ -150,6 +150,40 @@ __global__ __launch_bounds__(64 * COMPACT_ROWS_PER_BLOCK) void az_compact_policy
   if (lane == 0) count[row] = base;
 }
 
+// ---- allocation-free compact evaluation (az_eval_batch_compact_noalloc)
+// The dense policy between the evaluation and the compaction lives in this
+// file-scope device array instead of a buffer the library allocates: every
+// call on a GPU shares that GPU's copy (calls that overlap on one GPU race).
+// In host code `scratch` names a host-side stand-in, never the device memory:
+// host code uses the address hipGetSymbolAddress returns for the current
+// device, kept per device.
+constexpr size_t NOALLOC_FLOATS = (size_t)512 * 95 * AZ_SQUARES;  // 512 positions of the longest policy row
+static __device__ __align__(256) float scratch[NOALLOC_FLOATS];
+constexpr int NOALLOC_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[NOALLOC_MAX_DEVICES] = {};
+
+// The device address of `scratch` on the current device (looked up once per
+// device), or nullptr with the status in *st.
+float* scratch_for_current_device(int dev, int* st) {
+  if (dev < 0 || dev >= NOALLOC_MAX_DEVICES) {
+    *st = az_fail(AZ_ERR_UNSUPPORTED, "az_eval_batch_compact_noalloc: device index past 63");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      *st = az_fail(AZ_ERR_DEVICE, "az_eval_batch_compact_noalloc: hipGetSymbolAddress of the scratch array failed");
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = static_cast<float*>(ptr);
+  }
+  return g_scratch_ptr[dev];
+}
+
 int hip_err(hipError_t e, const char* what) {
   (void)hipGetLastError();
   return az_fail(e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation ? AZ_ERR_NOMEM : AZ_ERR_DEVICE, what);
@@ -494,6 +528,43 @@ int az_pipeline_drive(az_pipeline* p, int32_t workers, int32_t slots_per_worker,
   *seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
   for (int w = 0; w < workers; ++w)
     if (status[w] != AZ_OK) return az_fail(status[w], message[w].c_str());
+  return AZ_OK;
+}
+
+int az_eval_batch_compact_noalloc(az_net* net, const float* planes, const uint8_t* legal, int32_t B,
+                                  int32_t max_legal, float* policy, int32_t* legal_count, float* value,
+                                  void* stream) {
+  if (!net) return az_fail(AZ_ERR_INVALID_ARG, "az_eval_batch_compact_noalloc: NULL handle");
+  const az_layer_spec& sp = az_net_spec(net);
+  const int nm = az_spec_moves(sp);
+  if (max_legal < 1 || max_legal > nm)
+    return az_fail(AZ_ERR_INVALID_ARG, "az_eval_batch_compact_noalloc: max_legal must be 1..az_net_moves(net)");
+  if (B < 0 || B > sp.max_batch) return az_fail(AZ_ERR_INVALID_ARG, "az_eval_batch_compact_noalloc: B out of range");
+  if ((size_t)B * (size_t)nm > NOALLOC_FLOATS) {
+    char msg[200];
+    snprintf(msg, sizeof msg,
+             "az_eval_batch_compact_noalloc: B = %d needs %zu floats of scratch, more than its %zu (at most %zu positions "
+             "of %d policy cells)",
+             (int)B, (size_t)B * (size_t)nm, NOALLOC_FLOATS, NOALLOC_FLOATS / (size_t)nm, nm);
+    return az_fail(AZ_ERR_INVALID_ARG, msg);
+  }
+  if (B == 0) return AZ_OK;
+  if (!planes || !legal || !policy || !legal_count || !value)
+    return az_fail(AZ_ERR_INVALID_ARG, "az_eval_batch_compact_noalloc: NULL buffer");
+  if (((uintptr_t)policy | (uintptr_t)legal_count) & 3u)
+    return az_fail(AZ_ERR_INVALID_ARG, "az_eval_batch_compact_noalloc: policy and legal_count must be 4-byte aligned");
+  DeviceScope scope(az_net_device(net));
+  if (scope.err != hipSuccess) return hip_err(scope.err, "az_eval_batch_compact_noalloc: device");
+  int st = AZ_OK;
+  float* dense = scratch_for_current_device(az_net_device(net), &st);
+  if (!dense) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  st = az_eval_batch(net, planes, legal, B, dense, value, s);
+  if (st != AZ_OK) return st;
+  hipLaunchKernelGGL(az_compact_policy_kernel, dim3((B + COMPACT_ROWS_PER_BLOCK - 1) / COMPACT_ROWS_PER_BLOCK),
+                     dim3(64 * COMPACT_ROWS_PER_BLOCK), 0, s, dense, legal, B, nm, max_legal, policy, legal_count);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_err(e, "az_eval_batch_compact_noalloc: compaction launch");
   return AZ_OK;
 }
 
