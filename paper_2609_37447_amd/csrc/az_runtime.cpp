@@ -379,9 +379,12 @@ int choose_tiling(const az_net* n, int B) {
   // Measured on 20x128 (us per batch, large / one-board / medium tiling):
   // int8 768 boards 293 / 283 / 295, 896 boards 303 / 342 / 311, 1,024 boards
   // 327 / 368 / 338; bf16 640 boards 487 / 459 / 458, 768 boards 495 / 510 / 512.
+  // fp8: 640 boards 335 / 293 / 314, 768 boards 337 / 310 / 326, 896 boards
+  // 340 / 384 / 337, 1,024 boards 350 / 402 / 357.
   if (n->dtype == AZ_INT8) return B <= 768 ? 2 : 1;
   if (n->dtype == AZ_BF16) return B >= 768 ? 1 : 2;
-  if (n->dtype == AZ_FP8_E4M3 && B >= 1024) return 1;
+  if (B <= 768) return 2;
+  if (B >= 1024) return 1;
   return az_mfma_tiling_valid(F, 3) ? 3 : 1;
 }
 

@@ -523,12 +523,12 @@ def test_validate_gate_passes_faithful_and_flags_broken():
 
 def test_tiling_choice_per_dtype():
     # int8: the one-board tiling up to 768 boards (its 18-step weight ring makes it
-    # the fastest there), the large tiling beyond; fp8: one board below 512, medium
+    # the fastest there), the large tiling beyond; fp8: one board up to 768, medium
     # below 1024, large from 1024; bf16: one board below 768, large from 768
     import paper_2609_37447_amd as az
     shape, blob, ws, acs = _relu6_net()
     want = {"int8": {1: 2, 64: 2, 511: 2, 512: 2, 768: 2, 769: 1, 1024: 1},
-            "fp8": {64: 2, 511: 2, 512: 3, 1023: 3, 1024: 1},
+            "fp8": {64: 2, 511: 2, 768: 2, 769: 3, 1023: 3, 1024: 1},
             "bf16": {64: 2, 512: 2, 767: 2, 768: 1, 1024: 1}}
     for dtype, cases in want.items():
         if dtype == "bf16":
