@@ -27,15 +27,17 @@ def _int8_scales(w):
     return H.quant_scales(w.name, "int8")
 
 
-@pytest.mark.parametrize("wname", ["net20x128_int8_b1024", "deployed14x160_int8_b1024"])
-def test_noalloc_matches_pipeline_compact(wname):
+@pytest.mark.parametrize("wname,K", [("net20x128_int8_b1024", 256), ("deployed14x160_int8_b1024", 256),
+                                     ("net20x128_int8_b1024", 16)])
+def test_noalloc_matches_pipeline_compact(wname, K):
+    # K = 16: most rows have more legal moves than max_legal and are truncated
     import torch
 
     import paper_2609_37447_amd as az
     w = azgen.WORKLOADS[wname]
     blob = azgen.workload_weights(w)
     ws, acs = _int8_scales(w)
-    MB, K = 128, 256 if w.shape.n_moves > 256 else w.shape.n_moves
+    MB = 128
     _print(f"case noalloc {wname} max_batch={MB} max_legal={K}")
     spec = az.spec_from_shape(w.shape, MB)
     net = az.az_net_load(spec, blob, "int8", ws, acs)
@@ -72,8 +74,10 @@ def test_noalloc_matches_pipeline_compact(wname):
             assert np.array_equal(got_c, want_c), f"B={B} counts"
             assert np.array_equal(got_p, want_p), f"B={B} policy"
             assert np.array_equal(got_v, want_v), f"B={B} value"
-            # and the compact rows are the legal cells of the dense evaluation
+            # the counts are the true numbers of legal cells, also past max_legal
             assert np.array_equal(got_c, (legal != 0).sum(axis=1).astype(np.int32))
+            if K == 16:
+                assert (got_c > K).any()
             _print(f"  B={B}: equal to the pipeline, {int(got_c.max())} legal moves at most")
     finally:
         if pipe is not None:
